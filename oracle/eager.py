@@ -1,0 +1,133 @@
+"""Eager dense recurrence in float64 -- the plain definition the GPU path must reproduce.
+
+TEST INFRASTRUCTURE ONLY (see ``oracle/__init__.py``).
+
+The unified one-token decode step (Eq. 3) is
+
+    S_t = D(lambda_t) S_{t-1} + a_t b_t^T,      D(l) = diag(exp(l))   (Eq. 2)
+
+with the state S in R^{dk x dv}; D scales the *rows* (key dimension) of S.  Table 1
+instantiates (a_t, b_t) and the decay form per operator:
+
+    GDN   : head-wise scalar decay, a = k, b = beta (v - k^T S_old)
+    KDA   : per-key (diagonal) decay, same delta-rule pair as GDN
+    RWKV6 : per-key decay, a = k, b = v (no correction)
+
+Readings taken where the text is silent or ambiguous (each is listed in the design doc):
+
+* Correction state (delta rule).  Table 1 writes the old-state correction as
+  ``k_t^T S_{t-1}``.  The paper states the model semantics are unchanged and that the
+  correction is a *pre-update readout* (Sec. 3.1, "Append stage"); the published GDN
+  and KDA recurrences apply the correction to the decayed state
+  ``D(lambda_t) S_{t-1}``.  This oracle uses the decayed state by default; the literal
+  undecayed form is kept behind ``correction="undecayed"`` for diagnostics only.
+* Output timing.  GDN/KDA read out the post-update state ``o = q^T S_t`` (Eq. 3).
+  RWKV6 reads the pre-update state plus the per-head bonus ``u``:
+  ``o = r^T (S_{t-1} + diag(u) k v^T)`` -- the standard RWKV6 readout.
+* No query scaling is applied inside the step: any feature map or 1/sqrt(dk) is
+  absorbed into q by the caller (Sec. 2.1 folds the query feature map into q_t).
+
+Shapes (any leading batch dims ``...``, typically ``[N]`` heads):
+    S  [..., dk, dv]   q,k,r [..., dk]   v [..., dv]   beta [...]
+    lam [...] (GDN, scalar per head) or [..., dk] (KDA, RWKV6)
+    u  [..., dk] (RWKV6 bonus, broadcast from the per-head parameter [H, dk])
+"""
+
+import numpy as np
+
+OPS = ("gdn", "kda", "rwkv6")
+
+
+def _f64(x):
+    return np.asarray(x, dtype=np.float64)
+
+
+def row_decay(lam, dk, per_key):
+    """exp(lambda) as a per-row factor of shape [..., dk, 1] (Eq. 2).
+
+    ``per_key`` False: lam has shape [...] (one log-decay per head) and the value is
+    repeated over all dk rows (Sec. 2.1 represents scalar decay as a constant log-decay
+    vector).  ``per_key`` True: lam has shape [..., dk].
+    """
+    lam = _f64(lam)
+    if not per_key:
+        lam = np.broadcast_to(lam[..., None], lam.shape + (dk,))
+    elif lam.shape[-1] != dk:
+        raise ValueError("per-key log-decay must have a trailing dimension of dk")
+    return np.exp(lam)[..., :, None]
+
+
+def _readout(S, q):
+    """o_j = sum_i q_i S_ij  (q^T S)."""
+    return np.einsum("...i,...ij->...j", q, S)
+
+
+def gdn_kda_step(S, q, k, v, beta, lam, per_key, correction="decayed"):
+    """One delta-rule decode step: GDN (``per_key`` False) or KDA (``per_key`` True).
+
+    Eq. 3 with Table 1's GDN/KDA row.  Returns (S_t, o_t).
+    """
+    S, q, k, v, beta = map(_f64, (S, q, k, v, beta))
+    dk = S.shape[-2]
+    Sd = row_decay(lam, dk, per_key) * S                       # D(lambda_t) S_{t-1}
+    if correction == "decayed":
+        c = _readout(Sd, k)                           # k^T D(lambda_t) S_{t-1}
+    elif correction == "undecayed":                   # literal Table 1 text, diagnostic only
+        c = _readout(S, k)
+    else:
+        raise ValueError(correction)
+    b = beta[..., None] * (v - c)                     # b_t = beta_t (v_t - correction)
+    S_new = Sd + k[..., :, None] * b[..., None, :]    # + a_t b_t^T with a_t = k_t
+    o = _readout(S_new, q)                            # post-update readout, Eq. 3
+    return S_new, o
+
+
+def rwkv6_step(S, r, k, v, lam, u):
+    """One RWKV6 decode step: o = r^T (S_{t-1} + diag(u) k v^T); S_t = D(lambda) S + k v^T.
+
+    Table 1's RWKV6 row (diagonal decay, pair (k, v)) with the bonus readout.
+    """
+    S, r, k, v, u = map(_f64, (S, r, k, v, u))
+    dk = S.shape[-2]
+    bonus = np.sum(r * u * k, axis=-1)                # r^T diag(u) k
+    o = _readout(S, r) + bonus[..., None] * v         # pre-update readout + bonus
+    S_new = row_decay(lam, dk, True) * S + k[..., :, None] * v[..., None, :]
+    return S_new, o
+
+
+def eager_step(op, S, q, k, v, beta, lam, u=None, correction="decayed"):
+    """Dispatch one eager step for ``op`` in {"gdn", "kda", "rwkv6"}; returns (S_t, o_t).
+
+    For RWKV6 ``q`` carries the receptance r and ``beta`` is ignored.
+    """
+    if op in ("gdn", "kda"):
+        return gdn_kda_step(S, q, k, v, beta, lam, op == "kda", correction=correction)
+    if op == "rwkv6":
+        return rwkv6_step(S, q, k, v, lam, u)
+    raise ValueError(op)
+
+
+def eager_rollout(op, S0, steps, u=None, keep_states=False):
+    """Run the eager recurrence over a sequence of step inputs.
+
+    ``steps`` is an iterable of dicts with keys q, k, v, beta, lam (beta unused for
+    RWKV6).  Returns (outputs [T, ..., dv], final state, states or None).
+    """
+    S = _f64(S0)
+    outs, states = [], []
+    for st in steps:
+        S, o = eager_step(op, S, st["q"], st["k"], st["v"], st.get("beta"), st["lam"], u=u)
+        outs.append(o)
+        if keep_states:
+            states.append(S.copy())
+    return np.stack(outs), S, (states if keep_states else None)
+
+
+def rel_fro(x, ref):
+    """Relative Frobenius error ||x - ref|| / ||ref|| in float64 (the parity metric)."""
+    x, ref = _f64(x), _f64(ref)
+    den = np.linalg.norm(ref.ravel())
+    num = np.linalg.norm((x - ref).ravel())
+    if den == 0.0:
+        return float(num)
+    return float(num / den)
