@@ -1,0 +1,147 @@
+/*
+ * deltalog.h -- C ABI of libdeltalog.so: DeltaLog one-token decode state update for
+ * gated linear attention (GDN, KDA, RWKV6) on AMD Instinct MI355X (gfx950).
+ *
+ * The method (deferred materialisation of recurrent states, Sec. 3): the dense
+ * recurrent state of each (slot, head) is kept as a dense base S plus a bounded log of
+ * compact update factors.  Most decode steps read S once, replay the live log, emit
+ * the output and append one entry (Eq. 5); every M-th step folds the log and the
+ * current token back into S with a single dense write (Eq. 6).  The represented
+ * state is always Eq. 7:
+ *
+ *     S_logical = D(ell) S + sum_{i<L} D(ell - Lam_i) K_i U_i^T,   D(l) = diag(exp l)
+ *
+ * and equals the eager recurrence of Eq. 3 (Table 1 instantiations) in exact
+ * arithmetic.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Every data pointer is a DEVICE pointer (hipMalloc'd or a torch CUDA tensor),
+ *    owned by the caller.  The library never allocates, frees or synchronises; all
+ *    work is enqueued on the caller's `stream`, and buffers must stay alive until the
+ *    stream has executed it.  Calls on distinct buffers are re-entrant and thread-safe.
+ *  - Arrays are dense, row-major, with the shapes given below.  B = desc->num_slots,
+ *    H = desc->heads, C = desc->merge_interval - 1 (live-log capacity),
+ *    dl = 1 for GDN (one log-decay per head) and dl = dk for KDA/RWKV6 (per key).
+ *  - The state matrix of a head is dk x dv, rows indexed by the key dimension; the
+ *    decay D(.) scales rows (Eq. 2); outputs are o = x^T S (length dv).
+ *  - `slots` is a device int32 array of n distinct slot ids in [0, B): token row i
+ *    drives slot slots[i].  slots == NULL means the identity and requires n == B,
+ *    except that n == 0 is always a no-op: once the descriptor is valid and 0 <= n <= B
+ *    it returns DL_OK without looking at any pointer.
+ *    Duplicate ids in one call race (undefined).
+ *  - Token arrays are packed by token row: [n, H, ...].  Outputs are written by token
+ *    row, fp32, [n, H, dv].  `o` must not alias any input or state buffer.
+ *  - Every argument check happens on the host BEFORE any HIP call; a failing check
+ *    returns a negative dl_status and enqueues nothing (so the checks can be exercised
+ *    without a GPU).  A failed launch returns DL_E_HIP.  Corruption that only the
+ *    device can see (a slot id outside [0, B), a live length outside [0, C]) makes the
+ *    affected (slot, head) skip its work and ORs a code into *state->err (if non-NULL):
+ *    1 = bad slot id, 2 = live length out of range.
+ *  - Alignment: S, k_log, u_log, q, k, v and o must be 16-byte aligned; the other
+ *    float/int32 arrays 4-byte aligned.
+ *  - Supported shapes: dk, dv in {64, 128}; 1 <= M <= 64.
+ */
+#ifndef DELTALOG_H
+#define DELTALOG_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DL_ABI_VERSION 1
+#define DL_MAX_MERGE_INTERVAL 64
+
+typedef enum {
+  DL_OK = 0,
+  DL_E_NULL = -1,        /* a required pointer is NULL                                  */
+  DL_E_SHAPE = -2,       /* B, H, n or slot-list shape inconsistent                     */
+  DL_E_DTYPE = -3,       /* dtype combination not allowed                               */
+  DL_E_ALIGN = -4,       /* pointer not aligned as required                             */
+  DL_E_UNSUPPORTED = -5, /* dk/dv/M/op outside the supported set                        */
+  DL_E_HIP = -6,         /* the kernel launch failed                                    */
+  DL_E_VERSION = -7      /* desc->abi_version != DL_ABI_VERSION                         */
+} dl_status;
+
+typedef enum { DL_OP_GDN = 0, DL_OP_KDA = 1, DL_OP_RWKV6 = 2 } dl_op;
+typedef enum { DL_F32 = 0, DL_BF16 = 1 } dl_dtype;
+
+/* Problem description (host memory, read during the call only).
+ * Operators (Table 1): GDN = head-wise scalar decay with the delta-rule pair
+ * (k, beta (v - k^T D(lambda) S)); KDA = per-key decay with the same pair;
+ * RWKV6 = per-key decay with the pair (k, v) and the bonus readout
+ * o = r^T (S_{t-1} + diag(u) k v^T). */
+typedef struct {
+  int32_t abi_version;    /* must be DL_ABI_VERSION                                      */
+  int32_t op;             /* dl_op                                                       */
+  int32_t num_slots;      /* B >= 1: slots in the state buffers                          */
+  int32_t heads;          /* H >= 1                                                      */
+  int32_t dk, dv;         /* key / value head dims, each 64 or 128                       */
+  int32_t merge_interval; /* M in [1, 64]: one merge every M steps (Sec. 3.1); C = M-1   */
+  int32_t in_dtype;       /* dl_dtype of q/r, k, v; K_log stores exact copies of k       */
+  int32_t u_log_dtype;    /* dl_dtype of U_log: DL_F32 for GDN/KDA (corrected values),   */
+                          /* == in_dtype for RWKV6 (exact copies of v)                   */
+} dl_desc;
+
+/* DeltaLog physical state (Sec. 3.1 list of buffers), one entry per (slot, head). */
+typedef struct {
+  float*   S;        /* [B,H,dk,dv] fp32 dense base                                      */
+  float*   ell;      /* [B,H,dl]    fp32 cumulative log-decay since the last merge       */
+  void*    k_log;    /* [B,H,C,dk]  in_dtype   key-side factors   (may be NULL if C == 0) */
+  void*    u_log;    /* [B,H,C,dv]  u_log_dtype value-side factors (may be NULL if C == 0)*/
+  float*   lam_log;  /* [B,H,C,dl]  fp32 snapshot of ell per entry (may be NULL if C == 0)*/
+  int32_t* len;      /* [B,H]       live-log length L in [0, C]                          */
+  int32_t* err;      /* [1]         sticky device error word (see above); may be NULL    */
+} dl_state;
+
+/* Current-token inputs: the per-token interface of Eq. 3, one row per listed slot. */
+typedef struct {
+  const void*  q;    /* [n,H,dk] in_dtype: query (the receptance r for RWKV6)            */
+  const void*  k;    /* [n,H,dk] in_dtype: key, the key-side factor a_t                  */
+  const void*  v;    /* [n,H,dv] in_dtype: value                                         */
+  const float* beta; /* [n,H]    fp32 delta-rule write strength (GDN/KDA); NULL for RWKV6*/
+  const float* lam;  /* [n,H,dl] fp32 per-step log-decay lambda_t = log(alpha_t) <= 0     */
+  const float* u;    /* [H,dk]   fp32 RWKV6 bonus (per-head parameter); NULL otherwise   */
+} dl_token;
+
+/* Eager dense step (Eq. 3): S <- D(lambda) S + a b^T with the readout of Table 1, for
+ * the listed slots of a dense state S [B,H,dk,dv] fp32 (no log).  Writes o [n,H,dv].
+ * This is the baseline that reads and writes the whole state every token (Sec. 2.3).
+ * desc->merge_interval is validated but otherwise ignored. */
+int dl_eager_step(const dl_desc* desc, float* S, const dl_token* tok, float* o,
+                  const int32_t* slots, int32_t n, hipStream_t stream);
+
+/* One DeltaLog decode step (Alg. 1) for the listed slots: per (slot, head) read the
+ * base once, replay the live log, write the output, then append the factors
+ * (Eq. 5) if L < C, else merge log and token into the base (Eq. 6) and reset L and
+ * ell.  With M == 1 every step merges and the result equals dl_eager_step. */
+int dl_append_step(const dl_desc* desc, const dl_state* state, const dl_token* tok,
+                   float* o, const int32_t* slots, int32_t n, hipStream_t stream);
+
+/* Merge now, at any live length L in [0, C] (Eq. 6 is defined for general L).
+ * tok != NULL: consume the token exactly like the merge branch of dl_append_step and
+ *              write o (required).
+ * tok == NULL: flush -- materialise Eq. 7 into the base and reset (slot reuse,
+ *              eviction, checkpoint; Sec. 4 slot lifecycle); o is ignored. */
+int dl_merge(const dl_desc* desc, const dl_state* state, const dl_token* tok, float* o,
+             const int32_t* slots, int32_t n, hipStream_t stream);
+
+/* Read-only readout of the represented state (Eq. 7): o = x^T S_logical for a query
+ * x [n,H,dk] in in_dtype.  Mutates nothing.  (No RWKV6 bonus: there is no token.) */
+int dl_readout(const dl_desc* desc, const dl_state* state, const void* q, float* o,
+               const int32_t* slots, int32_t n, hipStream_t stream);
+
+/* Human-readable name of a dl_status value (static storage). */
+const char* dl_status_str(int status);
+
+/* DL_ABI_VERSION of the loaded library. */
+int dl_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DELTALOG_H */

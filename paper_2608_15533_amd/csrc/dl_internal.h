@@ -1,0 +1,41 @@
+// Internal interface between the C-ABI front end (abi.cpp) and the kernel translation
+// units (one per operator).  Plain C++ types only.
+#pragma once
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#include "deltalog.h"
+
+namespace dl {
+
+enum OpId { OP_GDN = DL_OP_GDN, OP_KDA = DL_OP_KDA, OP_RWKV6 = DL_OP_RWKV6 };
+enum ModeId { M_EAGER = 0, M_STEP = 1, M_MERGE = 2, M_FLUSH = 3, M_READOUT = 4 };
+
+// Everything a kernel needs, passed by value (all pointers are device pointers).
+struct KParams {
+  float* S;              // [B,H,dk,dv] dense base (or the eager dense state)
+  float* ell;            // [B,H,dl]
+  void* k_log;           // [B,H,C,dk]
+  void* u_log;           // [B,H,C,dv]
+  float* lam_log;        // [B,H,C,dl]
+  int32_t* len;          // [B,H]
+  int32_t* err;          // [1] or null
+  const void* q;         // [n,H,dk] (also the readout query)
+  const void* k;         // [n,H,dk]
+  const void* v;         // [n,H,dv]
+  const float* beta;     // [n,H]
+  const float* lam;      // [n,H,dl]
+  const float* u;        // [H,dk]
+  float* o;              // [n,H,dv]
+  const int32_t* slots;  // [n] or null (identity)
+  int32_t n, B, H, C;
+};
+
+// Launch the kernel for (op, mode, dk, dv, input dtype) with one workgroup per
+// (token row, head).  Returns the hipError_t of the launch.
+hipError_t launch_gdn(int mode, int dk, int dv, bool bf16, const KParams& p, hipStream_t s);
+hipError_t launch_kda(int mode, int dk, int dv, bool bf16, const KParams& p, hipStream_t s);
+hipError_t launch_rwkv6(int mode, int dk, int dv, bool bf16, const KParams& p, hipStream_t s);
+
+}  // namespace dl

@@ -1,0 +1,398 @@
+// DeltaLog decode kernels for gfx950 (CDNA4, wave64).
+//
+// One workgroup owns one (slot, head) state: a dk x dv fp32 matrix (64 KiB at 128x128).
+// Thread layout: NCG = dv/4 column groups (one float4 column slice each) times
+// NRG = dk/16 row groups; every thread keeps 16 rows x 4 columns of the state in
+// registers (rows rg, rg+NRG, ..., so one wave-wide float4 load covers whole
+// consecutive rows, 1 KiB contiguous).  The state is read from HBM exactly once
+// per step and, when the step materialises (merge / eager / flush), written back
+// exactly once from the same registers -- the read, the key-dimension reductions
+// and the write never leave the workgroup.  Because one workgroup owns all of a
+// head's value columns, the replay coefficients are computed once per (slot, head)
+// and the shared log metadata (K_log[L], Lam_log[L], ell, L) has a single writer
+// without any cross-workgroup finalisation (the ownership problem of Sec. 3.3).
+//
+// Modes (one template per mode; the per-slot append/merge branch of Alg. 1 is taken
+// on the device from that slot's live length):
+//   EAGER   Eq. 3 on a dense state (no log).
+//   STEP    Alg. 1: readout + replay, then append (Eq. 5) if L < C, else merge (Eq. 6).
+//   MERGE   the merge branch at the current L (a forced merge, any 0 <= L <= C).
+//   FLUSH   materialise Eq. 7 into the base and reset (no token).
+//   READOUT o = x^T (Eq. 7 state), no writes to the state.
+//
+// Per (slot, head) and step the arithmetic is (l' = ell + lambda):
+//   replay coefficient of entry i for a vector x:  g_i(x) = sum_r e^(l_r - Lam_i,r) x_r K_i,r
+//   base readout:   sum_r e^(l_r) x_r S_r,:      (l = l' for GDN/KDA, ell for RWKV6)
+//   correction c = base(k) + sum_i g_i(k) U_i ;  b = beta (v - c)             (GDN/KDA)
+//   output     o = base(q) + sum_i g_i(q) U_i + (q.k) b                       (GDN/KDA)
+//              o = base(r) + sum_i g_i(r) U_i + (r.(u*k)) v                   (RWKV6)
+//   merge      S <- diag(e^l') S + sum_i diag(e^(l'-Lam_i)) K_i U_i^T + k b^T  (Eq. 6)
+// Every decay factor is evaluated as exp of a log-decay *difference* (<= 0 in normal
+// use), never as a product of exp(l') and exp(-Lam_i).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "dl_internal.h"
+
+namespace dl {
+
+// ------------------------------------------------------------------ loads/stores
+__device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+__device__ __forceinline__ float ld1(const float* p) { return *p; }
+__device__ __forceinline__ float ld1(const uint16_t* p) { return __uint_as_float(uint32_t(*p) << 16); }
+
+__device__ __forceinline__ float4 ld4(const float* p) { return *reinterpret_cast<const float4*>(p); }
+__device__ __forceinline__ float4 ld4(const uint16_t* p) {
+  const uint2 w = *reinterpret_cast<const uint2*>(p);
+  return make_float4(bf_lo(w.x), bf_hi(w.x), bf_lo(w.y), bf_hi(w.y));
+}
+
+// Copy four elements verbatim (bit-exact log entries).
+__device__ __forceinline__ void cp4(float* d, const float* s) {
+  *reinterpret_cast<float4*>(d) = *reinterpret_cast<const float4*>(s);
+}
+__device__ __forceinline__ void cp4(uint16_t* d, const uint16_t* s) {
+  *reinterpret_cast<uint2*>(d) = *reinterpret_cast<const uint2*>(s);
+}
+
+__device__ __forceinline__ void st4(float* d, float4 v) { *reinterpret_cast<float4*>(d) = v; }
+
+__device__ __forceinline__ float4 f4(float a) { return make_float4(a, a, a, a); }
+__device__ __forceinline__ float4 operator+(float4 a, float4 b) {
+  return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w);
+}
+__device__ __forceinline__ float4 operator-(float4 a, float4 b) {
+  return make_float4(a.x - b.x, a.y - b.y, a.z - b.z, a.w - b.w);
+}
+__device__ __forceinline__ float4 operator*(float s, float4 a) {
+  return make_float4(s * a.x, s * a.y, s * a.z, s * a.w);
+}
+// a + s * b, written as separate fused multiply-adds per lane element.
+__device__ __forceinline__ float4 fma4(float s, float4 b, float4 a) {
+  return make_float4(fmaf(s, b.x, a.x), fmaf(s, b.y, a.y), fmaf(s, b.z, a.z), fmaf(s, b.w, a.w));
+}
+
+__device__ __forceinline__ float shfl_xor(float v, int m) { return __shfl_xor(v, m, 64); }
+
+// ------------------------------------------------------------------ configuration
+template <int OP, int DK, int DV, int MODE>
+struct Cfg {
+  static constexpr int RPT = 16;                 // state rows held per thread
+  static constexpr int NCG = DV / 4;             // float4 column groups
+  static constexpr int NRG = DK / RPT;           // row groups
+  static constexpr int NT = NCG * NRG;           // threads per workgroup
+  static constexpr int NW = NT / 64;             // waves per workgroup
+  static constexpr int DL = (OP == OP_GDN) ? 1 : DK;   // log-decay width
+  static constexpr int LPE = 16;                 // lanes per log entry (coefficient pass)
+  static constexpr int EPP = NT / LPE;           // log entries per coefficient pass
+  static constexpr int RPL = DK / LPE;           // key rows per lane (coefficient pass)
+  static constexpr int CH = 16;                  // log entries staged per merge chunk
+  static constexpr int KTS = CH + 4;             // LDS row stride of the staged K~ chunk
+  static constexpr bool DELTA = OP != OP_RWKV6;
+  static constexpr bool HAS_LOG = MODE != M_EAGER;
+  static constexpr bool HAS_TOKEN = MODE == M_EAGER || MODE == M_STEP || MODE == M_MERGE;
+  static constexpr bool READS_OUT = MODE != M_FLUSH;
+  static constexpr bool NEEDS_C = DELTA && HAS_TOKEN;
+  static constexpr bool CAN_MERGE = MODE != M_READOUT;
+  static constexpr bool MERGES_LOG = CAN_MERGE && HAS_LOG;
+  static_assert(NT % 64 == 0 && NT <= 256, "workgroup must be whole waves");
+  static_assert(64 % NCG == 0, "a wave must hold whole rows");
+  static_assert(NT % LPE == 0 && DK % LPE == 0, "coefficient pass layout");
+  static_assert(NT == (DV / 4) * (DK / 16), "launch bound must match the layout");
+};
+
+template <int OP, typename TIN>
+struct UType { using type = float; };          // GDN/KDA: U_log holds corrected values, fp32
+template <typename TIN>
+struct UType<OP_RWKV6, TIN> { using type = TIN; };  // RWKV6: U_log holds exact copies of v
+
+// ------------------------------------------------------------------ the kernel
+template <int OP, int DK, int DV, int MODE, typename TIN>
+__global__ __launch_bounds__((DV / 4) * (DK / 16))
+void deltalog_kernel(KParams p) {
+  using CF = Cfg<OP, DK, DV, MODE>;
+  using TU = typename UType<OP, TIN>::type;
+  constexpr int NT = CF::NT, NCG = CF::NCG, NRG = CF::NRG, RPT = CF::RPT, DL = CF::DL;
+
+  __shared__ float s_kf[DK];      // k (raw)
+  __shared__ float s_qf[DK];      // q or r (raw)
+  __shared__ float s_xk[DK];      // e^(l_r) k_r       (base correction vector)
+  __shared__ float s_xq[DK];      // e^(l_r) q_r       (base readout vector)
+  __shared__ float s_em[DK];      // e^(l'_r)          (materialisation row scale)
+  __shared__ float s_lr[DL];      // readout log-decay l
+  __shared__ float s_lm[DL];      // materialisation log-decay l'
+  __shared__ float s_gk[DL_MAX_MERGE_INTERVAL];
+  __shared__ float s_gq[DL_MAX_MERGE_INTERVAL];
+  __shared__ float s_red[CF::NW][2][DV];
+  __shared__ float s_dot[2];
+  __shared__ float s_kt[CF::MERGES_LOG ? DK * CF::KTS : 1];          // K~ chunk [DK][KTS]
+  __shared__ float4 s_u[CF::MERGES_LOG ? CF::CH * NCG : 1];          // U chunk  [CH][NCG]
+
+  const int tid = threadIdx.x;
+  const int H = p.H;
+  const int row = blockIdx.x / H;                 // token row
+  const int h = blockIdx.x - row * H;             // head
+  const int slot = p.slots ? p.slots[row] : row;
+  if (slot < 0 || slot >= p.B) {                  // uniform per workgroup
+    if (tid == 0 && p.err) atomicOr(p.err, 1);
+    return;
+  }
+  const size_t sh = size_t(slot) * H + h;         // state (slot, head) index
+  const size_t th = size_t(row) * H + h;          // token (row, head) index
+  const int C = p.C;
+
+  int L = 0;
+  if constexpr (CF::HAS_LOG) {
+    L = __builtin_amdgcn_readfirstlane(p.len[sh]);
+    if (L < 0 || L > C) {
+      if (tid == 0 && p.err) atomicOr(p.err, 2);
+      return;
+    }
+  }
+
+  // ---- 1. issue the state tile loads (the dominant HBM stream) -------------------
+  const int cg = tid % NCG;
+  const int rg = tid / NCG;
+  float* Sh = p.S + sh * size_t(DK) * DV;
+  float4 t[RPT];
+#pragma unroll
+  for (int j = 0; j < RPT; ++j) t[j] = ld4(Sh + size_t(rg + NRG * j) * DV + 4 * cg);
+
+  // ---- 2. per-row token vectors and decay factors (LDS) --------------------------
+  const TIN* kin = static_cast<const TIN*>(p.k) + th * DK;
+  const TIN* qin = static_cast<const TIN*>(p.q) + th * DK;
+  for (int r = tid; r < DK; r += NT) {
+    const int rd = (DL == 1) ? 0 : r;
+    float kf = 0.f, qf = 0.f, lam = 0.f, ell = 0.f;
+    if constexpr (CF::HAS_TOKEN) {
+      kf = ld1(kin + r);
+      lam = p.lam[th * DL + rd];
+    }
+    if constexpr (CF::READS_OUT) qf = ld1(qin + r);
+    if constexpr (CF::HAS_LOG) ell = p.ell[sh * DL + rd];
+    float lr, lm;
+    if constexpr (MODE == M_EAGER) {
+      lr = CF::DELTA ? lam : 0.f;   // delta rule reads the decayed state; RWKV6 the old one
+      lm = lam;
+    } else if constexpr (MODE == M_STEP || MODE == M_MERGE) {
+      lm = ell + lam;
+      lr = CF::DELTA ? lm : ell;
+    } else {                        // FLUSH, READOUT: the represented state as it stands
+      lr = ell;
+      lm = ell;
+    }
+    const float er = expf(lr);
+    s_kf[r] = kf;
+    s_qf[r] = qf;
+    s_xk[r] = er * kf;
+    s_xq[r] = er * qf;
+    s_em[r] = expf(lm);
+    if (r < DL) {
+      s_lr[r] = lr;
+      s_lm[r] = lm;
+    }
+  }
+  __syncthreads();
+
+  // ---- 3. dot products of the token (wave 0) and replay coefficients (all) -------
+  if constexpr (CF::HAS_TOKEN) {
+    if (tid < 64) {
+      float d = 0.f;
+      for (int r = tid; r < DK; r += 64) {
+        if constexpr (CF::DELTA) d = fmaf(s_qf[r], s_kf[r], d);                    // q.k
+        else d = fmaf(s_qf[r] * p.u[size_t(h) * DK + r], s_kf[r], d);            // r.(u*k)
+      }
+#pragma unroll
+      for (int m = 32; m >= 1; m >>= 1) d += shfl_xor(d, m);
+      if (tid == 0) s_dot[0] = d;
+    }
+  }
+  if constexpr (CF::HAS_LOG && CF::READS_OUT) {
+    const TIN* Kb = static_cast<const TIN*>(p.k_log) + sh * size_t(C) * DK;
+    const float* Lb = p.lam_log + sh * size_t(C) * DL;
+    const int e = tid / CF::LPE;
+    const int c = tid % CF::LPE;
+    for (int i0 = 0; i0 < L; i0 += CF::EPP) {    // uniform trip count
+      const int i = i0 + e;
+      float ak = 0.f, aq = 0.f;
+      if (i < L) {
+        const TIN* Ki = Kb + size_t(i) * DK + c * CF::RPL;
+        if constexpr (DL == 1) {
+          const float w = expf(s_lr[0] - Lb[i]);
+#pragma unroll
+          for (int x = 0; x < CF::RPL; ++x) {
+            const float kv = ld1(Ki + x);
+            const int r = c * CF::RPL + x;
+            ak = fmaf(kv, s_kf[r], ak);
+            aq = fmaf(kv, s_qf[r], aq);
+          }
+          ak *= w;
+          aq *= w;
+        } else {
+          const float* Li = Lb + size_t(i) * DK + c * CF::RPL;
+#pragma unroll
+          for (int x = 0; x < CF::RPL; ++x) {
+            const int r = c * CF::RPL + x;
+            const float wk = expf(s_lr[r] - Li[x]) * ld1(Ki + x);
+            ak = fmaf(wk, s_kf[r], ak);
+            aq = fmaf(wk, s_qf[r], aq);
+          }
+        }
+      }
+#pragma unroll
+      for (int m = CF::LPE / 2; m >= 1; m >>= 1) {
+        ak += shfl_xor(ak, m);
+        aq += shfl_xor(aq, m);
+      }
+      if (c == 0 && i < L) {
+        s_gk[i] = ak;
+        s_gq[i] = aq;
+      }
+    }
+  }
+  __syncthreads();
+
+  // ---- 4. base readouts from the registers + log replay, reduced over rows -------
+  float4 cv = f4(0.f), ov = f4(0.f);
+  if constexpr (CF::READS_OUT) {
+#pragma unroll
+    for (int j = 0; j < RPT; ++j) {
+      const int r = rg + NRG * j;
+      if constexpr (CF::NEEDS_C) cv = fma4(s_xk[r], t[j], cv);
+      ov = fma4(s_xq[r], t[j], ov);
+    }
+    if constexpr (CF::HAS_LOG) {
+      const TU* Ub = static_cast<const TU*>(p.u_log) + sh * size_t(C) * DV + 4 * cg;
+      for (int i = rg; i < L; i += NRG) {
+        const float4 uv = ld4(Ub + size_t(i) * DV);
+        if constexpr (CF::NEEDS_C) cv = fma4(s_gk[i], uv, cv);
+        ov = fma4(s_gq[i], uv, ov);
+      }
+    }
+    // Rows of one column group live in lanes NCG apart inside a wave, then across waves.
+#pragma unroll
+    for (int m = NCG; m < 64; m <<= 1) {
+      if constexpr (CF::NEEDS_C) {
+        cv.x += shfl_xor(cv.x, m); cv.y += shfl_xor(cv.y, m);
+        cv.z += shfl_xor(cv.z, m); cv.w += shfl_xor(cv.w, m);
+      }
+      ov.x += shfl_xor(ov.x, m); ov.y += shfl_xor(ov.y, m);
+      ov.z += shfl_xor(ov.z, m); ov.w += shfl_xor(ov.w, m);
+    }
+    if constexpr (CF::NW > 1) {
+      const int w = tid / 64, lane = tid % 64;
+      if (lane < NCG) {
+        if constexpr (CF::NEEDS_C) st4(&s_red[w][0][4 * cg], cv);
+        st4(&s_red[w][1][4 * cg], ov);
+      }
+      __syncthreads();
+      cv = f4(0.f);
+      ov = f4(0.f);
+#pragma unroll
+      for (int w2 = 0; w2 < CF::NW; ++w2) {
+        if constexpr (CF::NEEDS_C) cv = cv + *reinterpret_cast<const float4*>(&s_red[w2][0][4 * cg]);
+        ov = ov + *reinterpret_cast<const float4*>(&s_red[w2][1][4 * cg]);
+      }
+    }
+  }
+
+  // ---- 5. update factors and output ------------------------------------------------
+  float4 bv = f4(0.f);
+  if constexpr (CF::HAS_TOKEN) {
+    const float4 vv = ld4(static_cast<const TIN*>(p.v) + th * DV + 4 * cg);
+    if constexpr (CF::DELTA) {
+      bv = p.beta[th] * (vv - cv);          // b = beta (v - c)
+      ov = fma4(s_dot[0], bv, ov);          // + (q.k) b : post-update readout
+    } else {
+      bv = vv;                              // RWKV6: b = v
+      ov = fma4(s_dot[0], vv, ov);          // + (r.(u*k)) v : bonus
+    }
+  }
+  if constexpr (CF::READS_OUT) {
+    if (rg == 0) st4(p.o + th * DV + 4 * cg, ov);
+  }
+  if constexpr (MODE == M_READOUT) return;
+
+  // ---- 6a. append (Eq. 5): L < C in STEP mode --------------------------------------
+  if constexpr (MODE == M_STEP) {
+    if (L < C) {
+      const size_t ent = sh * size_t(C) + L;
+      TU* Ud = static_cast<TU*>(p.u_log) + ent * DV + 4 * cg;
+      if (rg == 0) {
+        if constexpr (CF::DELTA) st4(reinterpret_cast<float*>(Ud), bv);
+        else cp4(Ud, static_cast<const TIN*>(p.v) + th * DV + 4 * cg);
+      }
+      TIN* Kd = static_cast<TIN*>(p.k_log) + ent * DK;
+      constexpr int KCH = DK * int(sizeof(TIN)) / 16;   // 16-byte chunks of one key row
+      for (int x = tid; x < KCH; x += NT)
+        reinterpret_cast<uint4*>(Kd)[x] = reinterpret_cast<const uint4*>(kin)[x];
+      for (int x = tid; x < DL; x += NT) {
+        p.lam_log[ent * DL + x] = s_lm[x];
+        p.ell[sh * DL + x] = s_lm[x];
+      }
+      if (tid == 0) p.len[sh] = L + 1;
+      return;
+    }
+  }
+
+  // ---- 6b. materialise (Eq. 6 / Eq. 7 / Eq. 3) ---------------------------------------
+  if constexpr (CF::CAN_MERGE) {
+#pragma unroll
+    for (int j = 0; j < RPT; ++j) {
+      const int r = rg + NRG * j;
+      t[j] = s_em[r] * t[j];
+      if constexpr (CF::HAS_TOKEN) t[j] = fma4(s_kf[r], bv, t[j]);
+    }
+    if constexpr (CF::MERGES_LOG) {
+      const TIN* Kb = static_cast<const TIN*>(p.k_log) + sh * size_t(C) * DK;
+      const float* Lb = p.lam_log + sh * size_t(C) * DL;
+      const TU* Ub = static_cast<const TU*>(p.u_log) + sh * size_t(C) * DV;
+      for (int i0 = 0; i0 < L; i0 += CF::CH) {     // uniform trip count
+        const int n = min(CF::CH, L - i0);
+        __syncthreads();                            // previous chunk fully consumed
+        for (int x = tid; x < DK * CF::CH; x += NT) {
+          const int r = x % DK, ii = x / DK;
+          float val = 0.f;
+          if (ii < n) {
+            const int i = i0 + ii;
+            const float lam_i = Lb[size_t(i) * DL + ((DL == 1) ? 0 : r)];
+            val = expf(s_lm[(DL == 1) ? 0 : r] - lam_i) * ld1(Kb + size_t(i) * DK + r);
+          }
+          s_kt[r * CF::KTS + ii] = val;             // K~_i[r] = e^(l'_r - Lam_i,r) K_i[r]
+        }
+        for (int x = tid; x < CF::CH * NCG; x += NT) {
+          const int ii = x / NCG, c4 = x % NCG;
+          s_u[x] = (ii < n) ? ld4(Ub + size_t(i0 + ii) * DV + 4 * c4) : f4(0.f);
+        }
+        __syncthreads();
+        for (int ii = 0; ii < n; ii += 4) {          // zero-padded to a multiple of 4
+          const float4 u0 = s_u[(ii + 0) * NCG + cg];
+          const float4 u1 = s_u[(ii + 1) * NCG + cg];
+          const float4 u2 = s_u[(ii + 2) * NCG + cg];
+          const float4 u3 = s_u[(ii + 3) * NCG + cg];
+#pragma unroll
+          for (int j = 0; j < RPT; ++j) {
+            const int r = rg + NRG * j;
+            const float4 kt = *reinterpret_cast<const float4*>(&s_kt[r * CF::KTS + ii]);
+            t[j] = fma4(kt.x, u0, t[j]);
+            t[j] = fma4(kt.y, u1, t[j]);
+            t[j] = fma4(kt.z, u2, t[j]);
+            t[j] = fma4(kt.w, u3, t[j]);
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < RPT; ++j) st4(Sh + size_t(rg + NRG * j) * DV + 4 * cg, t[j]);
+    if constexpr (CF::HAS_LOG) {
+      for (int x = tid; x < DL; x += NT) p.ell[sh * DL + x] = 0.f;
+      if (tid == 0) p.len[sh] = 0;
+    }
+  }
+}
+
+}  // namespace dl

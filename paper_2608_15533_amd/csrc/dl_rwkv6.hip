@@ -1,0 +1,8 @@
+// RWKV6 instantiations of the DeltaLog decode kernels.
+#include "dl_launch.hpp"
+
+namespace dl {
+hipError_t launch_rwkv6(int mode, int dk, int dv, bool bf16, const KParams& p, hipStream_t s) {
+  return launch_op<OP_RWKV6>(mode, dk, dv, bf16, p, s);
+}
+}  // namespace dl

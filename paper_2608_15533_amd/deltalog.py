@@ -1,0 +1,232 @@
+"""ctypes binding of libdeltalog.so -- argument marshalling only.
+
+The entry points keep the C names (``dl_eager_step``, ``dl_append_step``, ``dl_merge``,
+``dl_readout``) and take torch CUDA tensors; each call checks layouts, builds the C
+structs and calls the library, which launches the HIP kernels on the current (or the
+given) stream.  No arithmetic of the method happens here.  PyTorch is used only to
+own device memory and to name the stream.
+
+Importing this module loads the library and raises ImportError when it has not been
+built -- there is no fallback path.
+"""
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libdeltalog.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(
+        f"{LIB_PATH} is missing: build it with `python -m paper_2608_15533_amd.build` "
+        "(the DeltaLog path has no non-HIP fallback)")
+
+_lib = ctypes.CDLL(LIB_PATH)
+
+# ----------------------------------------------------------------- constants (deltalog.h)
+DL_ABI_VERSION = 1
+DL_MAX_MERGE_INTERVAL = 64
+DL_OK, DL_E_NULL, DL_E_SHAPE, DL_E_DTYPE, DL_E_ALIGN, DL_E_UNSUPPORTED, DL_E_HIP, DL_E_VERSION = (
+    0, -1, -2, -3, -4, -5, -6, -7)
+DL_OP_GDN, DL_OP_KDA, DL_OP_RWKV6 = 0, 1, 2
+DL_F32, DL_BF16 = 0, 1
+OP_IDS = {"gdn": DL_OP_GDN, "kda": DL_OP_KDA, "rwkv6": DL_OP_RWKV6}
+DTYPE_IDS = {"f32": DL_F32, "bf16": DL_BF16}
+TORCH_DTYPES = {"f32": torch.float32, "bf16": torch.bfloat16}
+
+EXPORTED = ("dl_eager_step", "dl_append_step", "dl_merge", "dl_readout", "dl_status_str",
+            "dl_abi_version")
+
+
+class dl_desc(ctypes.Structure):
+    _fields_ = [("abi_version", ctypes.c_int32), ("op", ctypes.c_int32),
+                ("num_slots", ctypes.c_int32), ("heads", ctypes.c_int32),
+                ("dk", ctypes.c_int32), ("dv", ctypes.c_int32),
+                ("merge_interval", ctypes.c_int32), ("in_dtype", ctypes.c_int32),
+                ("u_log_dtype", ctypes.c_int32)]
+
+
+class dl_state(ctypes.Structure):
+    _fields_ = [("S", ctypes.c_void_p), ("ell", ctypes.c_void_p), ("k_log", ctypes.c_void_p),
+                ("u_log", ctypes.c_void_p), ("lam_log", ctypes.c_void_p),
+                ("len", ctypes.c_void_p), ("err", ctypes.c_void_p)]
+
+
+class dl_token(ctypes.Structure):
+    _fields_ = [("q", ctypes.c_void_p), ("k", ctypes.c_void_p), ("v", ctypes.c_void_p),
+                ("beta", ctypes.c_void_p), ("lam", ctypes.c_void_p), ("u", ctypes.c_void_p)]
+
+
+_P = ctypes.c_void_p
+_lib.dl_eager_step.argtypes = [ctypes.POINTER(dl_desc), _P, ctypes.POINTER(dl_token), _P, _P,
+                               ctypes.c_int32, _P]
+_lib.dl_append_step.argtypes = [ctypes.POINTER(dl_desc), ctypes.POINTER(dl_state),
+                                ctypes.POINTER(dl_token), _P, _P, ctypes.c_int32, _P]
+_lib.dl_merge.argtypes = [ctypes.POINTER(dl_desc), ctypes.POINTER(dl_state),
+                          ctypes.POINTER(dl_token), _P, _P, ctypes.c_int32, _P]
+_lib.dl_readout.argtypes = [ctypes.POINTER(dl_desc), ctypes.POINTER(dl_state), _P, _P, _P,
+                            ctypes.c_int32, _P]
+for _f in ("dl_eager_step", "dl_append_step", "dl_merge", "dl_readout", "dl_abi_version"):
+    getattr(_lib, _f).restype = ctypes.c_int
+_lib.dl_status_str.argtypes = [ctypes.c_int]
+_lib.dl_status_str.restype = ctypes.c_char_p
+
+lib = _lib
+
+
+class DeltaLogError(RuntimeError):
+    def __init__(self, status, where):
+        self.status = status
+        super().__init__(f"{where}: {dl_status_str(status)} ({status})")
+
+
+def dl_status_str(status):
+    return _lib.dl_status_str(int(status)).decode()
+
+
+def dl_abi_version():
+    return _lib.dl_abi_version()
+
+
+if dl_abi_version() != DL_ABI_VERSION:
+    raise ImportError(f"libdeltalog ABI {dl_abi_version()} != binding ABI {DL_ABI_VERSION}")
+
+
+# ----------------------------------------------------------------- descriptors
+def make_desc(op, B, H, dk, dv, M, in_dtype="bf16"):
+    """dl_desc for operator ``op`` ("gdn"/"kda"/"rwkv6") with merge interval M."""
+    u_dtype = in_dtype if op == "rwkv6" else "f32"
+    return dl_desc(DL_ABI_VERSION, OP_IDS[op], B, H, dk, dv, M, DTYPE_IDS[in_dtype],
+                   DTYPE_IDS[u_dtype])
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _need(t, name, dtype, shape, device=None):
+    if t is None:
+        raise ValueError(f"{name} is required")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if t.dtype != dtype:
+        raise ValueError(f"{name}: dtype {t.dtype}, expected {dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name}: shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+class DeltaLogState:
+    """Device buffers of the physical state (Sec. 3.1), allocated with torch.
+
+    S [B,H,dk,dv] f32, ell [B,H,dl] f32, k_log [B,H,C,dk] in_dtype, u_log [B,H,C,dv],
+    lam_log [B,H,C,dl] f32, len [B,H] int32, err [1] int32.  ``S`` starts as a copy of
+    ``S0`` (the prefill state); the log starts empty (Sec. 4 slot lifecycle).
+    """
+
+    def __init__(self, desc, S0=None, device="cuda"):
+        self.desc = desc
+        B, H, dk, dv, M = desc.num_slots, desc.heads, desc.dk, desc.dv, desc.merge_interval
+        C = M - 1
+        dl = 1 if desc.op == DL_OP_GDN else dk
+        in_t = torch.bfloat16 if desc.in_dtype == DL_BF16 else torch.float32
+        u_t = torch.bfloat16 if desc.u_log_dtype == DL_BF16 else torch.float32
+        f32 = dict(dtype=torch.float32, device=device)
+        self.S = torch.zeros((B, H, dk, dv), **f32) if S0 is None else S0.to(device=device, dtype=torch.float32).contiguous().clone()
+        self.ell = torch.zeros((B, H, dl), **f32)
+        self.k_log = torch.zeros((B, H, max(C, 0), dk), dtype=in_t, device=device)
+        self.u_log = torch.zeros((B, H, max(C, 0), dv), dtype=u_t, device=device)
+        self.lam_log = torch.zeros((B, H, max(C, 0), dl), **f32)
+        self.len = torch.zeros((B, H), dtype=torch.int32, device=device)
+        self.err = torch.zeros((1,), dtype=torch.int32, device=device)
+        self.struct = dl_state(_ptr(self.S), _ptr(self.ell),
+                               _ptr(self.k_log) if C > 0 else None,
+                               _ptr(self.u_log) if C > 0 else None,
+                               _ptr(self.lam_log) if C > 0 else None,
+                               _ptr(self.len), _ptr(self.err))
+
+    def buffers(self):
+        return dict(S=self.S, ell=self.ell, k_log=self.k_log, u_log=self.u_log,
+                    lam_log=self.lam_log, len=self.len, err=self.err)
+
+
+class Token:
+    """Device tensors of one decode step's inputs plus the dl_token struct over them."""
+
+    def __init__(self, desc, n, q, k, v, lam, beta=None, u=None):
+        H, dk, dv = desc.heads, desc.dk, desc.dv
+        dl = 1 if desc.op == DL_OP_GDN else dk
+        it = torch.bfloat16 if desc.in_dtype == DL_BF16 else torch.float32
+        _need(q, "q", it, (n, H, dk))
+        _need(k, "k", it, (n, H, dk))
+        _need(v, "v", it, (n, H, dv))
+        _need(lam, "lam", torch.float32, (n, H) if dl == 1 else (n, H, dl))
+        if desc.op == DL_OP_RWKV6:
+            _need(u, "u", torch.float32, (H, dk))
+        else:
+            _need(beta, "beta", torch.float32, (n, H))
+        self.n = n
+        self.tensors = (q, k, v, lam, beta, u)
+        self.struct = dl_token(_ptr(q), _ptr(k), _ptr(v), _ptr(beta), _ptr(lam), _ptr(u))
+
+
+def _stream(stream):
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    return getattr(stream, "cuda_stream", stream)
+
+
+def _rows(desc, slots, n):
+    if slots is None:
+        return None, desc.num_slots if n is None else n
+    _need(slots, "slots", torch.int32, (slots.numel(),))
+    return slots.data_ptr(), slots.numel()
+
+
+def _check(rc, where):
+    if rc != DL_OK:
+        raise DeltaLogError(rc, where)
+
+
+# ----------------------------------------------------------------- entry points
+def dl_eager_step(desc, S, tok, o, slots=None, stream=None):
+    """Eager dense step (Eq. 3) on S [B,H,dk,dv]; writes o [n,H,dv] f32."""
+    sp, n = _rows(desc, slots, tok.n)
+    _need(o, "o", torch.float32, (n, desc.heads, desc.dv))
+    _need(S, "S", torch.float32, (desc.num_slots, desc.heads, desc.dk, desc.dv))
+    _check(_lib.dl_eager_step(ctypes.byref(desc), _ptr(S), ctypes.byref(tok.struct), _ptr(o),
+                              sp, n, _stream(stream)), "dl_eager_step")
+
+
+def dl_append_step(desc, state, tok, o, slots=None, stream=None):
+    """One DeltaLog step (Alg. 1): append if L < C else merge; writes o [n,H,dv] f32."""
+    sp, n = _rows(desc, slots, tok.n)
+    _need(o, "o", torch.float32, (n, desc.heads, desc.dv))
+    _check(_lib.dl_append_step(ctypes.byref(desc), ctypes.byref(state.struct),
+                               ctypes.byref(tok.struct), _ptr(o), sp, n, _stream(stream)),
+           "dl_append_step")
+
+
+def dl_merge(desc, state, tok=None, o=None, slots=None, stream=None):
+    """Merge at the current L with the token (writes o), or flush when tok is None."""
+    sp, n = _rows(desc, slots, None if tok is None else tok.n)
+    if tok is not None:
+        _need(o, "o", torch.float32, (n, desc.heads, desc.dv))
+    _check(_lib.dl_merge(ctypes.byref(desc), ctypes.byref(state.struct),
+                         None if tok is None else ctypes.byref(tok.struct),
+                         _ptr(o) if tok is not None else None, sp, n, _stream(stream)),
+           "dl_merge")
+
+
+def dl_readout(desc, state, q, o, slots=None, stream=None):
+    """o = q^T S_logical (Eq. 7) for q [n,H,dk]; mutates nothing."""
+    n = q.shape[0]
+    sp, n = _rows(desc, slots, n)
+    it = torch.bfloat16 if desc.in_dtype == DL_BF16 else torch.float32
+    _need(q, "q", it, (n, desc.heads, desc.dk))
+    _need(o, "o", torch.float32, (n, desc.heads, desc.dv))
+    _check(_lib.dl_readout(ctypes.byref(desc), ctypes.byref(state.struct), _ptr(q), _ptr(o),
+                           sp, n, _stream(stream)), "dl_readout")

@@ -1,0 +1,167 @@
+"""The C-ABI library on a host without a GPU: it loads, exports every symbol the header
+declares, and rejects bad arguments before any HIP call (so nothing is launched).
+
+Fake device addresses are used throughout: every call here fails validation (or has
+n == 0), so no pointer is ever dereferenced and no kernel is enqueued."""
+
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2608_15533_amd import deltalog as D
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "deltalog.h")
+
+A = 0x10000000          # a fake, 256-byte aligned "device" address
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dl_[a-z_]+)\s*\(", text)))
+
+
+def test_header_functions_are_exported():
+    names = _declared_functions()
+    assert set(names) == set(D.EXPORTED)
+    out = subprocess.run(["nm", "-D", "--defined-only", D.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (dl_[a-z_]+)\b", out))
+    for n in names:
+        assert n in exported, n
+        assert hasattr(D.lib, n)
+
+
+def test_version_and_status_strings():
+    assert D.dl_abi_version() == D.DL_ABI_VERSION == 1
+    for code in range(0, -8, -1):
+        s = D.dl_status_str(code)
+        assert s.startswith("DL_") and s != "unknown dl_status"
+    assert D.dl_status_str(-99) == "unknown dl_status"
+
+
+def desc(**kw):
+    d = D.make_desc("gdn", 4, 2, 128, 128, 16, "bf16")
+    for k, v in kw.items():
+        setattr(d, k, v)
+    return d
+
+
+def state(**kw):
+    s = D.dl_state(A, A + 0x100000, A + 0x200000, A + 0x300000, A + 0x400000, A + 0x500000, None)
+    for k, v in kw.items():
+        setattr(s, k, v)
+    return s
+
+
+def token(**kw):
+    t = D.dl_token(A + 0x600000, A + 0x700000, A + 0x800000, A + 0x900000, A + 0xA00000, None)
+    for k, v in kw.items():
+        setattr(t, k, v)
+    return t
+
+
+def append(d, s=None, t=None, o=A + 0xB00000, slots=None, n=4):
+    return D.lib.dl_append_step(ctypes.byref(d), ctypes.byref(s or state()),
+                                ctypes.byref(t or token()), o, slots, n, None)
+
+
+def test_null_descriptor():
+    assert D.lib.dl_append_step(None, ctypes.byref(state()), ctypes.byref(token()), A, None, 4,
+                                None) == D.DL_E_NULL
+
+
+@pytest.mark.parametrize("field,value,code", [
+    ("abi_version", 2, D.DL_E_VERSION),
+    ("op", 3, D.DL_E_UNSUPPORTED),
+    ("dk", 96, D.DL_E_UNSUPPORTED),
+    ("dv", 256, D.DL_E_UNSUPPORTED),
+    ("merge_interval", 0, D.DL_E_UNSUPPORTED),
+    ("merge_interval", 65, D.DL_E_UNSUPPORTED),
+    ("num_slots", 0, D.DL_E_SHAPE),
+    ("heads", 0, D.DL_E_SHAPE),
+    ("in_dtype", 7, D.DL_E_DTYPE),
+    ("u_log_dtype", D.DL_BF16, D.DL_E_DTYPE),        # GDN U_log must be fp32
+])
+def test_descriptor_rejections(field, value, code):
+    assert append(desc(**{field: value})) == code
+
+
+def test_rwkv6_u_log_dtype_must_match_input():
+    d = D.make_desc("rwkv6", 4, 2, 64, 64, 16, "bf16")
+    d.u_log_dtype = D.DL_F32
+    assert append(d, t=token(beta=None, u=A + 0xC00000)) == D.DL_E_DTYPE
+
+
+def test_slot_list_rules():
+    assert append(desc(), n=5) == D.DL_E_SHAPE              # n > B
+    assert append(desc(), n=-1) == D.DL_E_SHAPE
+    assert append(desc(), n=3) == D.DL_E_SHAPE              # identity needs n == B
+    assert append(desc(), slots=A + 2, n=3) == D.DL_E_ALIGN
+
+
+@pytest.mark.parametrize("field", ["S", "ell", "len", "k_log", "u_log", "lam_log"])
+def test_state_nulls(field):
+    assert append(desc(), s=state(**{field: None})) == D.DL_E_NULL
+
+
+def test_log_buffers_optional_when_M_is_1():
+    """With M == 1 there is no log: NULL log buffers pass the state checks (the call then
+    stops at the misaligned output, which is checked after the state)."""
+    s = state(k_log=None, u_log=None, lam_log=None)
+    assert append(desc(merge_interval=1), s=s, o=A + 4) == D.DL_E_ALIGN
+    assert append(desc(merge_interval=2), s=s, o=A + 4) == D.DL_E_NULL
+
+
+@pytest.mark.parametrize("field", ["q", "k", "v", "lam", "beta"])
+def test_token_nulls(field):
+    assert append(desc(), t=token(**{field: None})) == D.DL_E_NULL
+
+
+def test_rwkv6_needs_bonus():
+    d = D.make_desc("rwkv6", 4, 2, 64, 64, 16, "bf16")
+    assert append(d, t=token(beta=None)) == D.DL_E_NULL
+
+
+@pytest.mark.parametrize("where,field,off", [
+    ("state", "S", 8), ("state", "k_log", 4), ("state", "u_log", 8), ("state", "ell", 2),
+    ("token", "q", 8), ("token", "k", 2), ("token", "v", 4), ("token", "lam", 1),
+])
+def test_alignment(where, field, off):
+    if where == "state":
+        s = state()
+        setattr(s, field, getattr(s, field) + off)
+        assert append(desc(), s=s) == D.DL_E_ALIGN
+    else:
+        t = token()
+        setattr(t, field, getattr(t, field) + off)
+        assert append(desc(), t=t) == D.DL_E_ALIGN
+
+
+def test_output_checks():
+    assert append(desc(), o=None) == D.DL_E_NULL
+    assert append(desc(), o=A + 4) == D.DL_E_ALIGN
+
+
+def test_zero_rows_is_a_no_op():
+    """n == 0 returns DL_OK without touching the GPU (this host has none)."""
+    assert append(desc(), slots=A, n=0) == D.DL_OK
+    d = desc()
+    assert D.lib.dl_eager_step(ctypes.byref(d), A, ctypes.byref(token()), A, A, 0, None) == D.DL_OK
+    assert D.lib.dl_merge(ctypes.byref(d), ctypes.byref(state()), None, None, A, 0, None) == D.DL_OK
+    assert D.lib.dl_readout(ctypes.byref(d), ctypes.byref(state()), A, A, A, 0, None) == D.DL_OK
+    assert append(desc(), slots=None, n=0) == D.DL_OK      # an empty list may be NULL
+    assert append(desc(), s=state(S=None), t=token(q=None), o=None, n=0) == D.DL_OK
+
+
+def test_other_entry_points_validate():
+    d = desc()
+    assert D.lib.dl_eager_step(ctypes.byref(d), None, ctypes.byref(token()), A, None, 4, None) == D.DL_E_NULL
+    assert D.lib.dl_merge(ctypes.byref(d), ctypes.byref(state()), ctypes.byref(token()), None,
+                          None, 4, None) == D.DL_E_NULL          # a merge with a token needs o
+    assert D.lib.dl_merge(ctypes.byref(d), None, None, None, None, 4, None) == D.DL_E_NULL
+    assert D.lib.dl_readout(ctypes.byref(d), ctypes.byref(state()), None, A, None, 4, None) == D.DL_E_NULL
+    assert D.lib.dl_readout(ctypes.byref(d), ctypes.byref(state()), A + 8, A, None, 4, None) == D.DL_E_ALIGN

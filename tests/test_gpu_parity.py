@@ -1,0 +1,79 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle on seeded inputs.
+
+Bar: relative Frobenius error <= 1e-4 for fp32 state, on every step's outputs, on the
+dense base after every merge, and on the base after a final flush.  Mid-size cases run
+every slot through the oracle; the full-size workloads (the launch configuration the
+benchmark times) run every slot on the GPU and a sample of slots through the oracle."""
+
+import numpy as np
+import pytest
+
+from paper_2608_15533_amd import workloads as W
+
+from gpu_harness import TOL_F32_STATE, Rollout, log
+
+pytestmark = pytest.mark.gpu
+
+
+def _check(r, what):
+    e_flush = r.flush_and_check()
+    log(f"{what}: max out err {r.err_out:.2e}, max state err {r.err_state:.2e} "
+        f"({r.n_state_checks} merge checks), flush {e_flush:.2e}")
+    assert r.device_error_word() == 0
+    assert r.err_out <= TOL_F32_STATE, what
+    assert r.err_state <= TOL_F32_STATE, what
+
+
+@pytest.mark.parametrize("in_dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("eager", [False, True], ids=["deltalog", "eager"])
+def test_gdn_b1_h2_d64_m8(in_dtype, eager):
+    """1 sequence, 2 heads, 64x64, M = 8, 64 steps: every output, 8 merges, flush."""
+    w = W.GDN_SMALL.with_(in_dtype=in_dtype)
+    r = Rollout(w, eager=eager).run()
+    assert eager or r.n_state_checks == w.steps // w.M
+    _check(r, f"gdn small {in_dtype} {'eager' if eager else 'deltalog'}")
+
+
+MID = [
+    ("gdn", W.GDN_B64, 16), ("kda", W.KDA_B128, 8), ("kda", W.KDA_B128, 16),
+    ("kda", W.KDA_B128, 32), ("rwkv6", W.RWKV6_B128, 16),
+]
+
+
+@pytest.mark.parametrize("op,w,M", MID, ids=[f"{o}_m{m}" for o, _, m in MID])
+@pytest.mark.parametrize("eager", [False, True], ids=["deltalog", "eager"])
+def test_mid_size_all_slots(op, w, M, eager):
+    """Full head shape and merge interval, 3 slots, 2M+5 steps (two merges and a ragged
+    partial cycle), every slot checked."""
+    r = Rollout(w, M=M, B=3, steps=2 * M + 5, eager=eager).run()
+    _check(r, f"{op} mid M={M} {'eager' if eager else 'deltalog'}")
+
+
+FULL = [
+    ("gdn_b64_h32_d128_m16", W.GDN_B64, 16, [0, 17, 63]),
+    ("kda_b128_h32_d128_m8", W.KDA_B128, 8, [1, 64, 127]),
+    ("kda_b128_h32_d128_m16", W.KDA_B128, 16, [2, 77, 126]),
+    ("kda_b128_h32_d128_m32", W.KDA_B128, 32, [3, 90, 125]),
+    ("rwkv6_b128_h40_d64_m16", W.RWKV6_B128, 16, [0, 55, 127]),
+]
+
+
+@pytest.mark.parametrize("name,w,M,sample", FULL, ids=[f[0] for f in FULL])
+def test_full_size_sampled(name, w, M, sample):
+    """The full workload (all slots, all steps) on the GPU; the oracle follows 3 slots."""
+    r = Rollout(w, M=M, sample=sample).run()
+    assert r.n_state_checks == w.steps // M
+    _check(r, f"{name} full")
+
+
+@pytest.mark.parametrize("layer", [0, 23])
+def test_serving_stack_layer_staggered(layer):
+    """One layer of the 24-layer stack: 256 slots whose logs start at staggered fill
+    offsets (partial-batch warm-up through slot lists), 128 steps; the oracle follows
+    slots with different offsets, so merges land on different steps."""
+    w = W.GDN_STACK
+    off = W.fill_offsets(w)
+    sample = [int(np.argmax(off == o)) for o in (0, 7, 15) if np.any(off == o)]
+    r = Rollout(w, layer=layer, sample=sample).run()
+    assert r.n_state_checks >= w.steps // w.M
+    _check(r, f"stack layer {layer} staggered")
