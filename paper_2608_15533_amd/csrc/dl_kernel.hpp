@@ -78,6 +78,58 @@ __device__ __forceinline__ float4 fma4(float s, float4 b, float4 a) {
 
 __device__ __forceinline__ float shfl_xor(float v, int m) { return __shfl_xor(v, m, 64); }
 
+// State-tile traffic.  The base is streamed once per step and not reused by this
+// workgroup, so by default its loads and stores carry the non-temporal hint.
+#ifndef DL_NT_STATE
+#define DL_NT_STATE 1
+#endif
+// Occupancy target (waves per SIMD) handed to the register allocator; 0 = compiler's choice.
+#ifndef DL_WAVES_PER_EU
+#define DL_WAVES_PER_EU 0
+#endif
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float4 ld_state(const float* p) {
+#if DL_NT_STATE
+  const f32x4 v = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p));
+  return make_float4(v.x, v.y, v.z, v.w);
+#else
+  return ld4(p);
+#endif
+}
+
+__device__ __forceinline__ void st_state(float* p, float4 v) {
+#if DL_NT_STATE
+  f32x4 w = {v.x, v.y, v.z, v.w};
+  __builtin_nontemporal_store(w, reinterpret_cast<f32x4*>(p));
+#else
+  st4(p, v);
+#endif
+}
+
+// N consecutive elements (N in {4, 8}) widened to fp32, loaded with 8/16-byte accesses.
+template <int N>
+__device__ __forceinline__ void ld_run(const float* p, float (&o)[N]) {
+#pragma unroll
+  for (int x = 0; x < N; x += 4) {
+    const float4 v = ld4(p + x);
+    o[x] = v.x; o[x + 1] = v.y; o[x + 2] = v.z; o[x + 3] = v.w;
+  }
+}
+template <int N>
+__device__ __forceinline__ void ld_run(const uint16_t* p, float (&o)[N]) {
+  if constexpr (N == 8) {
+    const uint4 w = *reinterpret_cast<const uint4*>(p);
+    o[0] = bf_lo(w.x); o[1] = bf_hi(w.x); o[2] = bf_lo(w.y); o[3] = bf_hi(w.y);
+    o[4] = bf_lo(w.z); o[5] = bf_hi(w.z); o[6] = bf_lo(w.w); o[7] = bf_hi(w.w);
+  } else {
+    static_assert(N == 4, "run length");
+    const uint2 w = *reinterpret_cast<const uint2*>(p);
+    o[0] = bf_lo(w.x); o[1] = bf_hi(w.x); o[2] = bf_lo(w.y); o[3] = bf_hi(w.y);
+  }
+}
+
 // ------------------------------------------------------------------ configuration
 template <int OP, int DK, int DV, int MODE>
 struct Cfg {
@@ -99,9 +151,12 @@ struct Cfg {
   static constexpr bool NEEDS_C = DELTA && HAS_TOKEN;
   static constexpr bool CAN_MERGE = MODE != M_READOUT;
   static constexpr bool MERGES_LOG = CAN_MERGE && HAS_LOG;
+  static constexpr bool REPLAYS = HAS_LOG && READS_OUT;   // readout of the live log
   static_assert(NT % 64 == 0 && NT <= 256, "workgroup must be whole waves");
   static_assert(64 % NCG == 0, "a wave must hold whole rows");
   static_assert(NT % LPE == 0 && DK % LPE == 0, "coefficient pass layout");
+  static_assert(NT >= DK, "one thread per key row in the prologue");
+  static_assert(RPL == 4 || RPL == 8, "coefficient pass run length");
   static_assert(NT == (DV / 4) * (DK / 16), "launch bound must match the layout");
 };
 
@@ -110,13 +165,23 @@ struct UType { using type = float; };          // GDN/KDA: U_log holds corrected
 template <typename TIN>
 struct UType<OP_RWKV6, TIN> { using type = TIN; };  // RWKV6: U_log holds exact copies of v
 
+#if DL_WAVES_PER_EU > 0
+#define DL_OCCUPANCY __attribute__((amdgpu_waves_per_eu(DL_WAVES_PER_EU)))
+#else
+#define DL_OCCUPANCY
+#endif
+
 // ------------------------------------------------------------------ the kernel
+// Every global load a workgroup needs is issued before its first barrier: the state
+// tile, the token rows, the first pass of log keys/snapshots and the first log values
+// of the replay; only the live length (and the slot id, for slot lists) precede them.
 template <int OP, int DK, int DV, int MODE, typename TIN>
-__global__ __launch_bounds__((DV / 4) * (DK / 16))
+__global__ __launch_bounds__((DV / 4) * (DK / 16)) DL_OCCUPANCY
 void deltalog_kernel(KParams p) {
   using CF = Cfg<OP, DK, DV, MODE>;
   using TU = typename UType<OP, TIN>::type;
   constexpr int NT = CF::NT, NCG = CF::NCG, NRG = CF::NRG, RPT = CF::RPT, DL = CF::DL;
+  constexpr int RPL = CF::RPL;
 
   __shared__ float s_kf[DK];      // k (raw)
   __shared__ float s_qf[DK];      // q or r (raw)
@@ -128,7 +193,7 @@ void deltalog_kernel(KParams p) {
   __shared__ float s_gk[DL_MAX_MERGE_INTERVAL];
   __shared__ float s_gq[DL_MAX_MERGE_INTERVAL];
   __shared__ float s_red[CF::NW][2][DV];
-  __shared__ float s_dot[2];
+  __shared__ float s_dotw[CF::NW];
   __shared__ float s_kt[CF::MERGES_LOG ? DK * CF::KTS : 1];          // K~ chunk [DK][KTS]
   __shared__ float4 s_u[CF::MERGES_LOG ? CF::CH * NCG : 1];          // U chunk  [CH][NCG]
 
@@ -144,36 +209,66 @@ void deltalog_kernel(KParams p) {
   const size_t sh = size_t(slot) * H + h;         // state (slot, head) index
   const size_t th = size_t(row) * H + h;          // token (row, head) index
   const int C = p.C;
-
   int L = 0;
-  if constexpr (CF::HAS_LOG) {
-    L = __builtin_amdgcn_readfirstlane(p.len[sh]);
-    if (L < 0 || L > C) {
-      if (tid == 0 && p.err) atomicOr(p.err, 2);
-      return;
-    }
-  }
+  if constexpr (CF::HAS_LOG) L = __builtin_amdgcn_readfirstlane(p.len[sh]);
+  const bool bad_len = L < 0 || L > C;
+  if (bad_len) L = 0;                             // keeps every address below in bounds
 
-  // ---- 1. issue the state tile loads (the dominant HBM stream) -------------------
+  // ---- 1. the state tile (the dominant HBM stream) --------------------------------
   const int cg = tid % NCG;
   const int rg = tid / NCG;
   float* Sh = p.S + sh * size_t(DK) * DV;
   float4 t[RPT];
 #pragma unroll
-  for (int j = 0; j < RPT; ++j) t[j] = ld4(Sh + size_t(rg + NRG * j) * DV + 4 * cg);
+  for (int j = 0; j < RPT; ++j) t[j] = ld_state(Sh + size_t(rg + NRG * j) * DV + 4 * cg);
 
-  // ---- 2. per-row token vectors and decay factors (LDS) --------------------------
+  if (bad_len) {
+    if (tid == 0 && p.err) atomicOr(p.err, 2);
+    return;
+  }
+
+  // ---- 2. register prefetch: token row values, log entries of the first pass -------
   const TIN* kin = static_cast<const TIN*>(p.k) + th * DK;
   const TIN* qin = static_cast<const TIN*>(p.q) + th * DK;
-  for (int r = tid; r < DK; r += NT) {
-    const int rd = (DL == 1) ? 0 : r;
-    float kf = 0.f, qf = 0.f, lam = 0.f, ell = 0.f;
+  const int r0 = tid;                              // this thread's key row in the prologue
+  float kf = 0.f, qf = 0.f, lam = 0.f, ell = 0.f, uf = 0.f;
+  if (r0 < DK) {
+    const int rd = (DL == 1) ? 0 : r0;
     if constexpr (CF::HAS_TOKEN) {
-      kf = ld1(kin + r);
+      kf = ld1(kin + r0);
       lam = p.lam[th * DL + rd];
+      if constexpr (!CF::DELTA) uf = p.u[size_t(h) * DK + r0];
     }
-    if constexpr (CF::READS_OUT) qf = ld1(qin + r);
+    if constexpr (CF::READS_OUT) qf = ld1(qin + r0);
     if constexpr (CF::HAS_LOG) ell = p.ell[sh * DL + rd];
+  }
+  float4 vv = f4(0.f);
+  float beta = 0.f;
+  if constexpr (CF::HAS_TOKEN) {
+    vv = ld4(static_cast<const TIN*>(p.v) + th * DV + 4 * cg);
+    if constexpr (CF::DELTA) beta = p.beta[th];
+  }
+  const TIN* Kb = static_cast<const TIN*>(p.k_log) + sh * size_t(C) * DK;
+  const float* Lb = p.lam_log + sh * size_t(C) * DL;
+  const TU* Ub = static_cast<const TU*>(p.u_log) + sh * size_t(C) * DV;
+  const int e_ = tid / CF::LPE;                   // coefficient pass: entry within the pass
+  const int c_ = tid % CF::LPE;                   //                   key-row run
+  float kr[RPL], lr_[(DL == 1) ? 1 : RPL];
+  if constexpr (CF::REPLAYS) {
+    if (e_ < L) {
+      ld_run<RPL>(Kb + size_t(e_) * DK + c_ * RPL, kr);
+      if constexpr (DL == 1) lr_[0] = Lb[e_];
+      else ld_run<RPL>(Lb + size_t(e_) * DK + c_ * RPL, lr_);
+    }
+  }
+  float4 up0 = f4(0.f), up1 = f4(0.f);            // first two replay values of this row group
+  if constexpr (CF::REPLAYS) {
+    if (rg < L) up0 = ld4(Ub + size_t(rg) * DV + 4 * cg);
+    if (rg + NRG < L) up1 = ld4(Ub + size_t(rg + NRG) * DV + 4 * cg);
+  }
+
+  // ---- 3. per-row decay factors (LDS) and the token dot product ---------------------
+  if (r0 < DK) {
     float lr, lm;
     if constexpr (MODE == M_EAGER) {
       lr = CF::DELTA ? lam : 0.f;   // delta rule reads the decayed state; RWKV6 the old one
@@ -186,58 +281,51 @@ void deltalog_kernel(KParams p) {
       lm = ell;
     }
     const float er = expf(lr);
-    s_kf[r] = kf;
-    s_qf[r] = qf;
-    s_xk[r] = er * kf;
-    s_xq[r] = er * qf;
-    s_em[r] = expf(lm);
-    if (r < DL) {
-      s_lr[r] = lr;
-      s_lm[r] = lm;
+    s_kf[r0] = kf;
+    s_qf[r0] = qf;
+    s_xk[r0] = er * kf;
+    s_xq[r0] = er * qf;
+    s_em[r0] = expf(lm);
+    if (r0 < DL) {
+      s_lr[r0] = lr;
+      s_lm[r0] = lm;
     }
+  }
+  if constexpr (CF::HAS_TOKEN) {
+    // q.k (delta rule, post-update readout) or r.(u*k) (RWKV6 bonus)
+    float d = CF::DELTA ? qf * kf : qf * uf * kf;
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) d += shfl_xor(d, m);
+    if ((tid & 63) == 0) s_dotw[tid >> 6] = d;
   }
   __syncthreads();
 
-  // ---- 3. dot products of the token (wave 0) and replay coefficients (all) -------
-  if constexpr (CF::HAS_TOKEN) {
-    if (tid < 64) {
-      float d = 0.f;
-      for (int r = tid; r < DK; r += 64) {
-        if constexpr (CF::DELTA) d = fmaf(s_qf[r], s_kf[r], d);                    // q.k
-        else d = fmaf(s_qf[r] * p.u[size_t(h) * DK + r], s_kf[r], d);            // r.(u*k)
-      }
-#pragma unroll
-      for (int m = 32; m >= 1; m >>= 1) d += shfl_xor(d, m);
-      if (tid == 0) s_dot[0] = d;
-    }
-  }
-  if constexpr (CF::HAS_LOG && CF::READS_OUT) {
-    const TIN* Kb = static_cast<const TIN*>(p.k_log) + sh * size_t(C) * DK;
-    const float* Lb = p.lam_log + sh * size_t(C) * DL;
-    const int e = tid / CF::LPE;
-    const int c = tid % CF::LPE;
-    for (int i0 = 0; i0 < L; i0 += CF::EPP) {    // uniform trip count
-      const int i = i0 + e;
+  // ---- 4. replay coefficients g_i(k), g_i(q) of the live entries --------------------
+  if constexpr (CF::REPLAYS) {
+    for (int i0 = 0; i0 < L; i0 += CF::EPP) {     // uniform trip count
+      const int i = i0 + e_;
       float ak = 0.f, aq = 0.f;
       if (i < L) {
-        const TIN* Ki = Kb + size_t(i) * DK + c * CF::RPL;
+        if (i0 > 0) {
+          ld_run<RPL>(Kb + size_t(i) * DK + c_ * RPL, kr);
+          if constexpr (DL == 1) lr_[0] = Lb[i];
+          else ld_run<RPL>(Lb + size_t(i) * DK + c_ * RPL, lr_);
+        }
         if constexpr (DL == 1) {
-          const float w = expf(s_lr[0] - Lb[i]);
 #pragma unroll
-          for (int x = 0; x < CF::RPL; ++x) {
-            const float kv = ld1(Ki + x);
-            const int r = c * CF::RPL + x;
-            ak = fmaf(kv, s_kf[r], ak);
-            aq = fmaf(kv, s_qf[r], aq);
+          for (int x = 0; x < RPL; ++x) {
+            const int r = c_ * RPL + x;
+            ak = fmaf(kr[x], s_kf[r], ak);
+            aq = fmaf(kr[x], s_qf[r], aq);
           }
+          const float w = expf(s_lr[0] - lr_[0]);
           ak *= w;
           aq *= w;
         } else {
-          const float* Li = Lb + size_t(i) * DK + c * CF::RPL;
 #pragma unroll
-          for (int x = 0; x < CF::RPL; ++x) {
-            const int r = c * CF::RPL + x;
-            const float wk = expf(s_lr[r] - Li[x]) * ld1(Ki + x);
+          for (int x = 0; x < RPL; ++x) {
+            const int r = c_ * RPL + x;
+            const float wk = expf(s_lr[r] - lr_[x]) * kr[x];
             ak = fmaf(wk, s_kf[r], ak);
             aq = fmaf(wk, s_qf[r], aq);
           }
@@ -248,15 +336,15 @@ void deltalog_kernel(KParams p) {
         ak += shfl_xor(ak, m);
         aq += shfl_xor(aq, m);
       }
-      if (c == 0 && i < L) {
+      if (c_ == 0 && i < L) {
         s_gk[i] = ak;
         s_gq[i] = aq;
       }
     }
+    __syncthreads();
   }
-  __syncthreads();
 
-  // ---- 4. base readouts from the registers + log replay, reduced over rows -------
+  // ---- 5. base readouts from the registers + log replay, reduced over rows -------
   float4 cv = f4(0.f), ov = f4(0.f);
   if constexpr (CF::READS_OUT) {
 #pragma unroll
@@ -266,9 +354,16 @@ void deltalog_kernel(KParams p) {
       ov = fma4(s_xq[r], t[j], ov);
     }
     if constexpr (CF::HAS_LOG) {
-      const TU* Ub = static_cast<const TU*>(p.u_log) + sh * size_t(C) * DV + 4 * cg;
-      for (int i = rg; i < L; i += NRG) {
-        const float4 uv = ld4(Ub + size_t(i) * DV);
+      if (rg < L) {
+        if constexpr (CF::NEEDS_C) cv = fma4(s_gk[rg], up0, cv);
+        ov = fma4(s_gq[rg], up0, ov);
+      }
+      if (rg + NRG < L) {
+        if constexpr (CF::NEEDS_C) cv = fma4(s_gk[rg + NRG], up1, cv);
+        ov = fma4(s_gq[rg + NRG], up1, ov);
+      }
+      for (int i = rg + 2 * NRG; i < L; i += NRG) {
+        const float4 uv = ld4(Ub + size_t(i) * DV + 4 * cg);
         if constexpr (CF::NEEDS_C) cv = fma4(s_gk[i], uv, cv);
         ov = fma4(s_gq[i], uv, ov);
       }
@@ -300,16 +395,18 @@ void deltalog_kernel(KParams p) {
     }
   }
 
-  // ---- 5. update factors and output ------------------------------------------------
+  // ---- 6. update factors and output ------------------------------------------------
   float4 bv = f4(0.f);
   if constexpr (CF::HAS_TOKEN) {
-    const float4 vv = ld4(static_cast<const TIN*>(p.v) + th * DV + 4 * cg);
+    float dot = 0.f;
+#pragma unroll
+    for (int w2 = 0; w2 < CF::NW; ++w2) dot += s_dotw[w2];
     if constexpr (CF::DELTA) {
-      bv = p.beta[th] * (vv - cv);          // b = beta (v - c)
-      ov = fma4(s_dot[0], bv, ov);          // + (q.k) b : post-update readout
+      bv = beta * (vv - cv);                // b = beta (v - c)
+      ov = fma4(dot, bv, ov);               // + (q.k) b : post-update readout
     } else {
       bv = vv;                              // RWKV6: b = v
-      ov = fma4(s_dot[0], vv, ov);          // + (r.(u*k)) v : bonus
+      ov = fma4(dot, vv, ov);               // + (r.(u*k)) v : bonus
     }
   }
   if constexpr (CF::READS_OUT) {
@@ -317,7 +414,7 @@ void deltalog_kernel(KParams p) {
   }
   if constexpr (MODE == M_READOUT) return;
 
-  // ---- 6a. append (Eq. 5): L < C in STEP mode --------------------------------------
+  // ---- 7a. append (Eq. 5): L < C in STEP mode --------------------------------------
   if constexpr (MODE == M_STEP) {
     if (L < C) {
       const size_t ent = sh * size_t(C) + L;
@@ -339,7 +436,7 @@ void deltalog_kernel(KParams p) {
     }
   }
 
-  // ---- 6b. materialise (Eq. 6 / Eq. 7 / Eq. 3) ---------------------------------------
+  // ---- 7b. materialise (Eq. 6 / Eq. 7 / Eq. 3) ---------------------------------------
   if constexpr (CF::CAN_MERGE) {
 #pragma unroll
     for (int j = 0; j < RPT; ++j) {
@@ -348,9 +445,6 @@ void deltalog_kernel(KParams p) {
       if constexpr (CF::HAS_TOKEN) t[j] = fma4(s_kf[r], bv, t[j]);
     }
     if constexpr (CF::MERGES_LOG) {
-      const TIN* Kb = static_cast<const TIN*>(p.k_log) + sh * size_t(C) * DK;
-      const float* Lb = p.lam_log + sh * size_t(C) * DL;
-      const TU* Ub = static_cast<const TU*>(p.u_log) + sh * size_t(C) * DV;
       for (int i0 = 0; i0 < L; i0 += CF::CH) {     // uniform trip count
         const int n = min(CF::CH, L - i0);
         __syncthreads();                            // previous chunk fully consumed
@@ -387,7 +481,7 @@ void deltalog_kernel(KParams p) {
       }
     }
 #pragma unroll
-    for (int j = 0; j < RPT; ++j) st4(Sh + size_t(rg + NRG * j) * DV + 4 * cg, t[j]);
+    for (int j = 0; j < RPT; ++j) st_state(Sh + size_t(rg + NRG * j) * DV + 4 * cg, t[j]);
     if constexpr (CF::HAS_LOG) {
       for (int x = tid; x < DL; x += NT) p.ell[sh * DL + x] = 0.f;
       if (tid == 0) p.len[sh] = 0;

@@ -16,7 +16,8 @@ import os
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libdeltalog.so")
+# DELTALOG_LIB selects another build of the same library (e.g. a tuning variant).
+LIB_PATH = os.environ.get("DELTALOG_LIB") or os.path.join(_HERE, "libdeltalog.so")
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(
