@@ -83,32 +83,51 @@ __device__ __forceinline__ float shfl_xor(float v, int m) { return __shfl_xor(v,
 #ifndef DL_NT_STATE
 #define DL_NT_STATE 1
 #endif
+// Log keys of the first coefficient pass / the first replay values of each row group
+// are loaded before the first barrier (1) or where they are used (0).
+#ifndef DL_PREFETCH_KEYS
+#define DL_PREFETCH_KEYS 1
+#endif
+#ifndef DL_PREFETCH_U
+#define DL_PREFETCH_U 1
+#endif
+// Per-key log snapshots of the first coefficient pass are loaded before the first
+// barrier (1) or right after it (0, fewer live registers).
+#ifndef DL_PREFETCH_PER_KEY
+#define DL_PREFETCH_PER_KEY 0
+#endif
 // Occupancy target (waves per SIMD) handed to the register allocator; 0 = compiler's choice.
 #ifndef DL_WAVES_PER_EU
 #define DL_WAVES_PER_EU 0
 #endif
 
-typedef float f32x4 __attribute__((ext_vector_type(4)));
+// The state tile of one (slot, head) is addressed through a buffer resource: the
+// head's base address lives in scalar registers, each lane keeps one 32-bit offset and
+// the row blocks differ by a scalar offset, so no per-row 64-bit addresses occupy
+// vector registers between the load and the store.  The resource covers exactly the
+// head's dk x dv floats; the hardware drops accesses outside it.
+constexpr int kStateCachePolicy = DL_NT_STATE ? 2 : 0;   // 2 = non-temporal
+constexpr int kRawBufferFlags = 0x00020000;                // 32-bit data format, raw access
 
-__device__ __forceinline__ float4 ld_state(const float* p) {
-#if DL_NT_STATE
-  const f32x4 v = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p));
-  return make_float4(v.x, v.y, v.z, v.w);
-#else
-  return ld4(p);
-#endif
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t state_rsrc(float* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(base, 0, int(bytes), kRawBufferFlags);
 }
 
-__device__ __forceinline__ void st_state(float* p, float4 v) {
-#if DL_NT_STATE
-  f32x4 w = {v.x, v.y, v.z, v.w};
-  __builtin_nontemporal_store(w, reinterpret_cast<f32x4*>(p));
-#else
-  st4(p, v);
-#endif
+__device__ __forceinline__ float4 ld_state(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+  const auto w = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, kStateCachePolicy);
+  return make_float4(__uint_as_float(w[0]), __uint_as_float(w[1]), __uint_as_float(w[2]),
+                     __uint_as_float(w[3]));
 }
 
-// N consecutive elements (N in {4, 8}) widened to fp32, loaded with 8/16-byte accesses.
+__device__ __forceinline__ void st_state(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff,
+                                         float4 v) {
+  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+  const u32x4 w = {__float_as_uint(v.x), __float_as_uint(v.y), __float_as_uint(v.z),
+                   __float_as_uint(v.w)};
+  __builtin_amdgcn_raw_buffer_store_b128(w, r, voff, soff, kStateCachePolicy);
+}
+
+// N consecutive elements (N a multiple of 8) widened to fp32, loaded with 16-byte accesses.
 template <int N>
 __device__ __forceinline__ void ld_run(const float* p, float (&o)[N]) {
 #pragma unroll
@@ -119,14 +138,12 @@ __device__ __forceinline__ void ld_run(const float* p, float (&o)[N]) {
 }
 template <int N>
 __device__ __forceinline__ void ld_run(const uint16_t* p, float (&o)[N]) {
-  if constexpr (N == 8) {
-    const uint4 w = *reinterpret_cast<const uint4*>(p);
-    o[0] = bf_lo(w.x); o[1] = bf_hi(w.x); o[2] = bf_lo(w.y); o[3] = bf_hi(w.y);
-    o[4] = bf_lo(w.z); o[5] = bf_hi(w.z); o[6] = bf_lo(w.w); o[7] = bf_hi(w.w);
-  } else {
-    static_assert(N == 4, "run length");
-    const uint2 w = *reinterpret_cast<const uint2*>(p);
-    o[0] = bf_lo(w.x); o[1] = bf_hi(w.x); o[2] = bf_lo(w.y); o[3] = bf_hi(w.y);
+  static_assert(N % 8 == 0, "run length");
+#pragma unroll
+  for (int x = 0; x < N; x += 8) {
+    const uint4 w = *reinterpret_cast<const uint4*>(p + x);
+    o[x + 0] = bf_lo(w.x); o[x + 1] = bf_hi(w.x); o[x + 2] = bf_lo(w.y); o[x + 3] = bf_hi(w.y);
+    o[x + 4] = bf_lo(w.z); o[x + 5] = bf_hi(w.z); o[x + 6] = bf_lo(w.w); o[x + 7] = bf_hi(w.w);
   }
 }
 
@@ -139,8 +156,8 @@ struct Cfg {
   static constexpr int NT = NCG * NRG;           // threads per workgroup
   static constexpr int NW = NT / 64;             // waves per workgroup
   static constexpr int DL = (OP == OP_GDN) ? 1 : DK;   // log-decay width
-  static constexpr int LPE = 16;                 // lanes per log entry (coefficient pass)
-  static constexpr int EPP = NT / LPE;           // log entries per coefficient pass
+  static constexpr int EPP = 16;                 // log entries per coefficient pass
+  static constexpr int LPE = NT / EPP;           // lanes per log entry (coefficient pass)
   static constexpr int RPL = DK / LPE;           // key rows per lane (coefficient pass)
   static constexpr int CH = 16;                  // log entries staged per merge chunk
   static constexpr int KTS = CH + 4;             // LDS row stride of the staged K~ chunk
@@ -156,7 +173,8 @@ struct Cfg {
   static_assert(64 % NCG == 0, "a wave must hold whole rows");
   static_assert(NT % LPE == 0 && DK % LPE == 0, "coefficient pass layout");
   static_assert(NT >= DK, "one thread per key row in the prologue");
-  static_assert(RPL == 4 || RPL == 8, "coefficient pass run length");
+  static_assert(RPL == 8 || RPL == 16, "coefficient pass run length");
+  static_assert(LPE <= 64 && 64 % LPE == 0, "an entry's lanes share one wave");
   static_assert(NT == (DV / 4) * (DK / 16), "launch bound must match the layout");
 };
 
@@ -209,19 +227,27 @@ void deltalog_kernel(KParams p) {
   const size_t sh = size_t(slot) * H + h;         // state (slot, head) index
   const size_t th = size_t(row) * H + h;          // token (row, head) index
   const int C = p.C;
-  int L = 0;
-  if constexpr (CF::HAS_LOG) L = __builtin_amdgcn_readfirstlane(p.len[sh]);
-  const bool bad_len = L < 0 || L > C;
-  if (bad_len) L = 0;                             // keeps every address below in bounds
+  // The live length is read through the scalar path (its own wait counter); it is
+  // first used only after the tile loads below have been issued.
+  int L_raw = 0;
+  if constexpr (CF::HAS_LOG) L_raw = p.len[sh];
 
   // ---- 1. the state tile (the dominant HBM stream) --------------------------------
   const int cg = tid % NCG;
   const int rg = tid / NCG;
-  float* Sh = p.S + sh * size_t(DK) * DV;
+  const auto srs = state_rsrc(p.S + sh * size_t(DK) * DV, DK * DV * 4);
+  const uint32_t toff = uint32_t(rg * DV + 4 * cg) * 4;   // this lane's byte offset in a row block
+  constexpr uint32_t kRowBlock = NRG * DV * 4;             // bytes between row j and row j+1 of a lane
   float4 t[RPT];
 #pragma unroll
-  for (int j = 0; j < RPT; ++j) t[j] = ld_state(Sh + size_t(rg + NRG * j) * DV + 4 * cg);
+  for (int j = 0; j < RPT; ++j) t[j] = ld_state(srs, toff, j * kRowBlock);
+  // Keep every use of the live length (and the branches on it) behind the tile loads,
+  // so the tile is in flight while the length comes back.
+  asm volatile("" ::: "memory");
 
+  int L = __builtin_amdgcn_readfirstlane(L_raw);
+  const bool bad_len = L < 0 || L > C;
+  if (bad_len) L = 0;                             // keeps every address below in bounds
   if (bad_len) {
     if (tid == 0 && p.err) atomicOr(p.err, 2);
     return;
@@ -254,7 +280,7 @@ void deltalog_kernel(KParams p) {
   const int e_ = tid / CF::LPE;                   // coefficient pass: entry within the pass
   const int c_ = tid % CF::LPE;                   //                   key-row run
   float kr[RPL], lr_[(DL == 1) ? 1 : RPL];
-  if constexpr (CF::REPLAYS) {
+  if constexpr (CF::REPLAYS && DL_PREFETCH_KEYS && (DL == 1 || DL_PREFETCH_PER_KEY)) {
     if (e_ < L) {
       ld_run<RPL>(Kb + size_t(e_) * DK + c_ * RPL, kr);
       if constexpr (DL == 1) lr_[0] = Lb[e_];
@@ -262,7 +288,7 @@ void deltalog_kernel(KParams p) {
     }
   }
   float4 up0 = f4(0.f), up1 = f4(0.f);            // first two replay values of this row group
-  if constexpr (CF::REPLAYS) {
+  if constexpr (CF::REPLAYS && DL_PREFETCH_U) {
     if (rg < L) up0 = ld4(Ub + size_t(rg) * DV + 4 * cg);
     if (rg + NRG < L) up1 = ld4(Ub + size_t(rg + NRG) * DV + 4 * cg);
   }
@@ -306,7 +332,7 @@ void deltalog_kernel(KParams p) {
       const int i = i0 + e_;
       float ak = 0.f, aq = 0.f;
       if (i < L) {
-        if (i0 > 0) {
+        if (i0 > 0 || !DL_PREFETCH_KEYS || (DL != 1 && !DL_PREFETCH_PER_KEY)) {
           ld_run<RPL>(Kb + size_t(i) * DK + c_ * RPL, kr);
           if constexpr (DL == 1) lr_[0] = Lb[i];
           else ld_run<RPL>(Lb + size_t(i) * DK + c_ * RPL, lr_);
@@ -322,7 +348,7 @@ void deltalog_kernel(KParams p) {
           ak *= w;
           aq *= w;
         } else {
-#pragma unroll
+#pragma unroll 2
           for (int x = 0; x < RPL; ++x) {
             const int r = c_ * RPL + x;
             const float wk = expf(s_lr[r] - lr_[x]) * kr[x];
@@ -354,15 +380,15 @@ void deltalog_kernel(KParams p) {
       ov = fma4(s_xq[r], t[j], ov);
     }
     if constexpr (CF::HAS_LOG) {
-      if (rg < L) {
+      if (DL_PREFETCH_U && rg < L) {
         if constexpr (CF::NEEDS_C) cv = fma4(s_gk[rg], up0, cv);
         ov = fma4(s_gq[rg], up0, ov);
       }
-      if (rg + NRG < L) {
+      if (DL_PREFETCH_U && rg + NRG < L) {
         if constexpr (CF::NEEDS_C) cv = fma4(s_gk[rg + NRG], up1, cv);
         ov = fma4(s_gq[rg + NRG], up1, ov);
       }
-      for (int i = rg + 2 * NRG; i < L; i += NRG) {
+      for (int i = rg + (DL_PREFETCH_U ? 2 * NRG : 0); i < L; i += NRG) {
         const float4 uv = ld4(Ub + size_t(i) * DV + 4 * cg);
         if constexpr (CF::NEEDS_C) cv = fma4(s_gk[i], uv, cv);
         ov = fma4(s_gq[i], uv, ov);
@@ -448,6 +474,7 @@ void deltalog_kernel(KParams p) {
       for (int i0 = 0; i0 < L; i0 += CF::CH) {     // uniform trip count
         const int n = min(CF::CH, L - i0);
         __syncthreads();                            // previous chunk fully consumed
+#pragma unroll 2
         for (int x = tid; x < DK * CF::CH; x += NT) {
           const int r = x % DK, ii = x / DK;
           float val = 0.f;
@@ -481,7 +508,7 @@ void deltalog_kernel(KParams p) {
       }
     }
 #pragma unroll
-    for (int j = 0; j < RPT; ++j) st_state(Sh + size_t(rg + NRG * j) * DV + 4 * cg, t[j]);
+    for (int j = 0; j < RPT; ++j) st_state(srs, toff, j * kRowBlock, t[j]);
     if constexpr (CF::HAS_LOG) {
       for (int x = tid; x < DL; x += NT) p.ell[sh * DL + x] = 0.f;
       if (tid == 0) p.len[sh] = 0;
