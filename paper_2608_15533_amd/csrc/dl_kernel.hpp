@@ -174,6 +174,7 @@ struct Cfg {
   static_assert(NT % LPE == 0 && DK % LPE == 0, "coefficient pass layout");
   static_assert(NT >= DK, "one thread per key row in the prologue");
   static_assert(RPL == 8 || RPL == 16, "coefficient pass run length");
+  static_assert(CH == EPP, "the first merge chunk is staged by the first coefficient pass");
   static_assert(LPE <= 64 && 64 % LPE == 0, "an entry's lanes share one wave");
   static_assert(NT == (DV / 4) * (DK / 16), "launch bound must match the layout");
 };
@@ -293,6 +294,17 @@ void deltalog_kernel(KParams p) {
     if (rg + NRG < L) up1 = ld4(Ub + size_t(rg + NRG) * DV + 4 * cg);
   }
 
+  // Does this (slot, head) materialise in this launch?  (Uniform per workgroup.)
+  const bool merging = MODE == M_MERGE || MODE == M_FLUSH || MODE == M_EAGER ||
+                       (MODE == M_STEP && L == C);
+  if constexpr (CF::MERGES_LOG) {
+    // The first chunk of log values is staged by the replay below; entries at or past L
+    // in that chunk must read as zero in the merge contraction.
+    if (merging)
+      for (int x = tid; x < CF::CH * NCG; x += NT)
+        if (x / NCG >= L) s_u[x] = f4(0.f);
+  }
+
   // ---- 3. per-row decay factors (LDS) and the token dot product ---------------------
   if (r0 < DK) {
     float lr, lm;
@@ -327,9 +339,13 @@ void deltalog_kernel(KParams p) {
   __syncthreads();
 
   // ---- 4. replay coefficients g_i(k), g_i(q) of the live entries --------------------
+  // A merging workgroup also writes the first chunk of decayed keys
+  // K~_i[r] = e^(l'_r - Lam_i,r) K_i[r] to LDS here, from the same loads (for the delta
+  // rule the merge decay l' equals the readout decay; RWKV6 reads at ell, merges at l').
   if constexpr (CF::REPLAYS) {
     for (int i0 = 0; i0 < L; i0 += CF::EPP) {     // uniform trip count
       const int i = i0 + e_;
+      const bool stage = CF::MERGES_LOG && merging && i0 == 0;
       float ak = 0.f, aq = 0.f;
       if (i < L) {
         if (i0 > 0 || !DL_PREFETCH_KEYS || (DL != 1 && !DL_PREFETCH_PER_KEY)) {
@@ -347,6 +363,10 @@ void deltalog_kernel(KParams p) {
           const float w = expf(s_lr[0] - lr_[0]);
           ak *= w;
           aq *= w;
+          if (stage) {
+#pragma unroll
+            for (int x = 0; x < RPL; ++x) s_kt[(c_ * RPL + x) * CF::KTS + e_] = w * kr[x];
+          }
         } else {
 #pragma unroll 2
           for (int x = 0; x < RPL; ++x) {
@@ -354,8 +374,12 @@ void deltalog_kernel(KParams p) {
             const float wk = expf(s_lr[r] - lr_[x]) * kr[x];
             ak = fmaf(wk, s_kf[r], ak);
             aq = fmaf(wk, s_qf[r], aq);
+            if (stage) s_kt[r * CF::KTS + e_] = CF::DELTA ? wk : expf(s_lm[r] - lr_[x]) * kr[x];
           }
         }
+      } else if (stage) {
+#pragma unroll
+        for (int x = 0; x < RPL; ++x) s_kt[(c_ * RPL + x) * CF::KTS + e_] = 0.f;
       }
 #pragma unroll
       for (int m = CF::LPE / 2; m >= 1; m >>= 1) {
@@ -380,18 +404,24 @@ void deltalog_kernel(KParams p) {
       ov = fma4(s_xq[r], t[j], ov);
     }
     if constexpr (CF::HAS_LOG) {
+      // Each log value row is read by exactly one row group; a merging workgroup keeps
+      // the first chunk of them in LDS for the merge contraction.
+      const bool stage_u = CF::MERGES_LOG && merging;
       if (DL_PREFETCH_U && rg < L) {
         if constexpr (CF::NEEDS_C) cv = fma4(s_gk[rg], up0, cv);
         ov = fma4(s_gq[rg], up0, ov);
+        if (stage_u && rg < CF::CH) s_u[rg * NCG + cg] = up0;
       }
       if (DL_PREFETCH_U && rg + NRG < L) {
         if constexpr (CF::NEEDS_C) cv = fma4(s_gk[rg + NRG], up1, cv);
         ov = fma4(s_gq[rg + NRG], up1, ov);
+        if (stage_u && rg + NRG < CF::CH) s_u[(rg + NRG) * NCG + cg] = up1;
       }
       for (int i = rg + (DL_PREFETCH_U ? 2 * NRG : 0); i < L; i += NRG) {
         const float4 uv = ld4(Ub + size_t(i) * DV + 4 * cg);
         if constexpr (CF::NEEDS_C) cv = fma4(s_gk[i], uv, cv);
         ov = fma4(s_gq[i], uv, ov);
+        if (stage_u && i < CF::CH) s_u[i * NCG + cg] = uv;
       }
     }
     // Rows of one column group live in lanes NCG apart inside a wave, then across waves.
@@ -473,7 +503,8 @@ void deltalog_kernel(KParams p) {
     if constexpr (CF::MERGES_LOG) {
       for (int i0 = 0; i0 < L; i0 += CF::CH) {     // uniform trip count
         const int n = min(CF::CH, L - i0);
-        __syncthreads();                            // previous chunk fully consumed
+        __syncthreads();                            // previous chunk consumed / chunk 0 visible
+        if (CF::REPLAYS && i0 == 0) goto contract;  // chunk 0 was staged during the replay
 #pragma unroll 2
         for (int x = tid; x < DK * CF::CH; x += NT) {
           const int r = x % DK, ii = x / DK;
@@ -490,6 +521,7 @@ void deltalog_kernel(KParams p) {
           s_u[x] = (ii < n) ? ld4(Ub + size_t(i0 + ii) * DV + 4 * c4) : f4(0.f);
         }
         __syncthreads();
+      contract:
         for (int ii = 0; ii < n; ii += 4) {          // zero-padded to a multiple of 4
           const float4 u0 = s_u[(ii + 0) * NCG + cg];
           const float4 u1 = s_u[(ii + 1) * NCG + cg];
