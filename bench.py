@@ -43,7 +43,25 @@ def parse():
     ap.add_argument("--replicas", type=int, default=8)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a plain device-to-device copy of MIB MiB (5 times); used to "
+                         "scale the HBM byte counters of a profiler run")
     return ap.parse_args()
+
+
+def copy_calibration(mib):
+    """A plain copy kernel of known size: counters read on it give the scale factor
+    between the profiler's FETCH_SIZE / WRITE_SIZE and bytes actually moved."""
+    import torch
+    n = mib * 2**20 // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes_read": n * 4, "bytes_written": n * 4,
+                      "launches": 5}), flush=True)
 
 
 def cpu_baseline(w, budget_s):
@@ -76,6 +94,9 @@ def cpu_baseline(w, budget_s):
 
 def main():
     args = parse()
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}): the decode state "
               "update has no cross-GPU step; run with --gpus 1.", file=sys.stderr)
@@ -123,60 +144,74 @@ def main():
         for k in range(k0, k0 + nsteps):
             for r in range(R):
                 if events is not None:
-                    events.append(torch.cuda.Event(enable_timing=True))
-                    events[-1].record(stream)
+                    a = torch.cuda.Event(enable_timing=True)
+                    a.record(stream)
                 rc = fn(*argtab[r][k % POOL])
                 if rc != 0:
                     raise D.DeltaLogError(rc, fn.__name__)
+                if events is not None:
+                    b = torch.cuda.Event(enable_timing=True)
+                    b.record(stream)
+                    events.append((a, b))
 
     def timed(fn, argtab):
+        """W untimed steps, then K timed steps bracketed by synchronize + HIP events on
+        the launch stream; returns elapsed ms (no per-launch events inside)."""
         run(fn, argtab, 0, WU)
         torch.cuda.synchronize()
-        evs = []
         t0 = torch.cuda.Event(enable_timing=True)
-        t0.record(stream)
-        run(fn, argtab, WU, K, evs)
         t1 = torch.cuda.Event(enable_timing=True)
+        t0.record(stream)
+        run(fn, argtab, WU, K)
         t1.record(stream)
         torch.cuda.synchronize()
-        total_ms = t0.elapsed_time(t1)
-        marks = evs + [t1]
-        durs = np.array([marks[i].elapsed_time(marks[i + 1]) for i in range(len(evs))])
-        return total_ms, durs.reshape(K, R)
+        return t0.elapsed_time(t1)
+
+    def per_launch(fn, argtab, k0, nsteps):
+        """A separate pass with an event pair around every launch (per-phase split)."""
+        evs = []
+        run(fn, argtab, k0, nsteps, evs)
+        torch.cuda.synchronize()
+        return np.array([a.elapsed_time(b) for a, b in evs]).reshape(nsteps, R)
 
     # ------------------------------------------------------------------ DeltaLog
-    dl_ms, dl_durs = timed(app, app_args)
-    for s in states:
-        assert int(s.err.item()) == 0
+    dl_ms = timed(app, app_args)
     heads = w.B * w.H
     Ls = [(WU + k) % w.M for k in range(K)]           # live length at each timed step
     step_bytes = np.array([T.step_bytes(w.op, w.dk, w.dv, w.M, L, w.in_dtype).total * heads
                            for L in Ls])
-    launch_bytes = np.repeat(step_bytes[:, None], R, axis=1)
+    n_launch = K * R
     dl_tok = w.B * R * K / (dl_ms * 1e-3)
-    achieved = launch_bytes.sum() / (dl_durs.sum() * 1e-3) / 1e9
+    avg_launch_us = dl_ms * 1e3 / n_launch
+    bytes_per_launch = float(step_bytes.mean())
+    achieved = bytes_per_launch / (avg_launch_us * 1e-6) / 1e9
 
+    # per-phase split: one more full cycle per replica, every launch bracketed
+    k0 = WU + K
+    PH = 2 * w.M
+    ph_durs = per_launch(app, app_args, k0, PH)
+    for s in states:
+        assert int(s.err.item()) == 0
     phases = {}
     for L in range(w.M):
-        sel = np.array([l == L for l in Ls])
-        if not sel.any():
-            continue
-        us = float(dl_durs[sel].mean() * 1e3)
+        sel = np.array([(k0 + k) % w.M == L for k in range(PH)])
+        us = float(ph_durs[sel].mean() * 1e3)
         b = T.step_bytes(w.op, w.dk, w.dv, w.M, L, w.in_dtype).total * heads
-        name = "merge" if L == w.M - 1 else f"append_L{L}"
+        name = "merge_L%d" % L if L == w.M - 1 else f"append_L{L}"
         phases[name] = {"us": round(us, 2), "GB/s": round(b / (us * 1e-6) / 1e9, 1)}
-    app_sel = np.array([l < w.M - 1 for l in Ls])
-    app_us = float(dl_durs[app_sel].mean() * 1e3)
-    app_bytes = float(launch_bytes[app_sel].mean())
-    mrg_sel = ~app_sel
-    mrg_us = float(dl_durs[mrg_sel].mean() * 1e3) if mrg_sel.any() else None
-    mrg_bytes = float(launch_bytes[mrg_sel].mean()) if mrg_sel.any() else None
+    app_sel = np.array([(k0 + k) % w.M < w.M - 1 for k in range(PH)])
+    app_us = float(ph_durs[app_sel].mean() * 1e3)
+    app_bytes = float(np.mean([T.step_bytes(w.op, w.dk, w.dv, w.M, (k0 + k) % w.M, w.in_dtype).total
+                               for k in range(PH) if app_sel[k]]) * heads)
+    mrg_us = float(ph_durs[~app_sel].mean() * 1e3)
+    mrg_bytes = T.merge_bytes(w.op, w.dk, w.dv, w.M - 1, w.in_dtype).total * heads
 
     # ------------------------------------------------------------------ eager baseline
-    eg_ms, eg_durs = timed(eag, eag_args)
+    eg_ms = timed(eag, eag_args)
     eg_tok = w.B * R * K / (eg_ms * 1e-3)
     eg_bytes = T.eager_bytes(w.op, w.dk, w.dv, w.in_dtype).total * heads
-    eg_gbs = eg_bytes / (eg_durs.mean() * 1e-3) / 1e9
+    eg_us = eg_ms * 1e3 / n_launch
+    eg_gbs = eg_bytes / (eg_us * 1e-6) / 1e9
 
     state_mib = w.B * w.H * w.dk * w.dv * 4 / 2**20
     res = {
@@ -210,19 +245,22 @@ def main():
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": None,
-            "avg_launch_us": round(float(dl_durs.mean() * 1e3), 3),
-            "algorithmic_bytes_per_launch": round(float(launch_bytes.mean()), 1),
+            "avg_launch_us": round(avg_launch_us, 3),
+            "algorithmic_bytes_per_launch": round(bytes_per_launch, 1),
+            "duration_source": "HIP events around the timed region / launches",
         },
         "phases": {
-            "append": {"us": round(app_us, 2), "GB/s": round(app_bytes / (app_us * 1e-6) / 1e9, 1)},
-            "merge": None if mrg_us is None else
-            {"us": round(mrg_us, 2), "GB/s": round(mrg_bytes / (mrg_us * 1e-6) / 1e9, 1)},
+            "source": "separate pass, HIP event pair around each launch",
+            "append": {"us": round(app_us, 2), "GB/s": round(app_bytes / (app_us * 1e-6) / 1e9, 1),
+                       "frac": round(app_bytes / (app_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)},
+            "merge": {"us": round(mrg_us, 2), "GB/s": round(mrg_bytes / (mrg_us * 1e-6) / 1e9, 1),
+                      "frac": round(mrg_bytes / (mrg_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)},
             "by_live_length": phases,
         },
         "eager": {
             "tokens_per_s": round(eg_tok, 1),
             "ms_per_step": round(eg_ms / K, 5),
-            "us_per_launch": round(float(eg_durs.mean() * 1e3), 3),
+            "us_per_launch": round(eg_us, 3),
             "GB/s": round(eg_gbs, 1),
             "frac": round(eg_gbs / HBM_PEAK_GBS, 4),
         },

@@ -147,6 +147,8 @@ __device__ __forceinline__ void ld_run(const uint16_t* p, float (&o)[N]) {
   }
 }
 
+constexpr uint32_t kXcds = 8;   // accelerator complex dies of an MI355X
+
 // ------------------------------------------------------------------ configuration
 template <int OP, int DK, int DV, int MODE>
 struct Cfg {
@@ -218,8 +220,16 @@ void deltalog_kernel(KParams p) {
 
   const int tid = threadIdx.x;
   const int H = p.H;
-  const int row = blockIdx.x / H;                 // token row
-  const int h = blockIdx.x - row * H;             // head
+  // Workgroups are dispatched round-robin over the 8 XCDs (each with its own L2).  Map
+  // them so that XCD x owns a contiguous range of (row, head) pairs: the 4-byte
+  // per-head metadata (ell, L, scalar log-decay snapshots) and token scalars of
+  // neighbouring heads then share L2 sectors instead of being written back partially
+  // by eight different caches.
+  uint32_t lin = blockIdx.x;
+  const uint32_t nblk = gridDim.x;
+  if (nblk % kXcds == 0) lin = (lin % kXcds) * (nblk / kXcds) + lin / kXcds;
+  const int row = int(lin) / H;                   // token row
+  const int h = int(lin) - row * H;               // head
   const int slot = p.slots ? p.slots[row] : row;
   if (slot < 0 || slot >= p.B) {                  // uniform per workgroup
     if (tid == 0 && p.err) atomicOr(p.err, 1);
