@@ -1,26 +1,36 @@
 """Decode state-update throughput of the DeltaLog HIP path on one MI355X.
 
-    python bench.py [--steps K] [--warmup W] [--replicas R] [--gpus 1] [--no-cpu-baseline]
+    python bench.py [--workload NAME] [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
 
-Workload: GDN delta-rule decode, 64 sequences x 32 heads, dk = dv = 128, fp32 state,
-bf16 q/k/v, merge interval M = 16 (one merge every 16 steps).  R independent copies of
-that layer's state (default 8, 1.2 GiB in all) are stepped in turn, like consecutive
-layers of a model, so the working set is far larger than the 256 MB last-level cache
-and every step streams its state from HBM.  A step is one decode token through all R
-layer states (R launches of dl_append_step); the reported value is per-layer
-token-updates per second, B * R * K / elapsed.  Token inputs come from a pool of 16
-pre-generated seeded steps cycled over the run (their values do not change the cost).
+Default workload: GDN delta-rule decode, 64 sequences x 32 heads, dk = dv = 128, fp32
+state, bf16 q/k/v, merge interval M = 16.  R = 8 independent copies of that layer's
+state (1.2 GiB in all) are stepped in turn, like consecutive layers of a model, so the
+working set is far larger than the 256 MB last-level cache and every step streams its
+state from HBM.  A step is one decode token through all R layer states (R launches of
+dl_append_step); the reported value is per-layer token-updates per second,
+B * R * K / elapsed.  Other workloads (--workload): KDA 128x32x128^2 at M in {8,16,32}
+(R = 4), RWKV6 128x40x64^2 at M = 16 (R = 12), and the 24-layer GDN stack of 256
+sequences with staggered log fill (R = 24 layers; value = 256 * K / elapsed).
 
-The JSON line also carries: the eager dense baseline (dl_eager_step on the same
-replicas), the per-phase split (append at each live length, merge), the roofline entry
-of the dominant kernel (algorithmic bytes of each launch over its duration measured
-with HIP events on the launch stream), and the fp64 CPU oracle timed on a bounded
-sample on this host.
+Token inputs come from a pool of 16 seeded steps of the workload generator, cycled over
+the run; initial states are drawn on the device (seeded torch normal, std 0.02).  The
+values do not change the cost of any kernel.
+
+Besides the contract fields the JSON line carries: the eager dense baseline
+(dl_eager_step on the same states), the per-phase split (append at each live length,
+merge; a separate pass with an event pair around every launch), the roofline entry of
+the dominant kernel (algorithmic bytes of the average launch over its average duration,
+the duration taken from HIP events around the timed region on the launch stream), the
+HBM traffic of that kernel from the committed counter profile when the kernel sources
+still match it, and the fp64 CPU oracle timed on a bounded sample on this host.
 """
 
 import argparse
+import glob
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -35,12 +45,25 @@ HBM_PEAK_GBS = 8000.0
 POOL = 16
 
 
+def workloads():
+    from paper_2608_15533_amd import workloads as W
+    return {
+        "gdn_b64_h32_d128_m16": (W.GDN_B64, 8),
+        "kda_b128_h32_d128_m8": (W.kda_with_merge_interval(8), 4),
+        "kda_b128_h32_d128_m16": (W.kda_with_merge_interval(16), 4),
+        "kda_b128_h32_d128_m32": (W.kda_with_merge_interval(32), 4),
+        "rwkv6_b128_h40_d64_m16": (W.RWKV6_B128, 12),
+        "gdn_stack24_b256_h32_d128_m16": (W.GDN_STACK, 24),
+    }
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--workload", default="gdn_b64_h32_d128_m16", choices=sorted(workloads()))
     ap.add_argument("--steps", type=int, default=256)
     ap.add_argument("--warmup", type=int, default=32)
-    ap.add_argument("--replicas", type=int, default=8)
+    ap.add_argument("--replicas", type=int, default=0, help="layer states (0: workload default)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -64,30 +87,63 @@ def copy_calibration(mib):
                       "launches": 5}), flush=True)
 
 
+def kernel_source_hash():
+    """sha256 over the kernel sources and the public header (any change invalidates
+    counter figures taken earlier)."""
+    files = sorted(glob.glob(os.path.join(ROOT, "paper_2608_15533_amd", "csrc", "*")))
+    files.append(os.path.join(ROOT, "include", "deltalog.h"))
+    h = hashlib.sha256()
+    for f in files:
+        h.update(os.path.basename(f).encode())
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def counter_traffic(workload):
+    """HBM bytes per launch of the dominant kernel from the committed counter profile,
+    or None when there is none or the kernel sources changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", f"{workload}_hbm_counters.txt")
+    if not os.path.exists(path):
+        return None, "no counter profile"
+    m = re.search(r"^TRAFFIC_JSON (\{.*\})$", open(path).read(), flags=re.M)
+    if not m:
+        return None, "counter profile has no TRAFFIC_JSON line"
+    d = json.loads(m.group(1))
+    if d.get("kernel_source_hash") != kernel_source_hash():
+        return None, "kernel sources changed since the counters were taken"
+    return d["step_kernel_bytes_per_launch"], os.path.relpath(path, ROOT)
+
+
 def cpu_baseline(w, budget_s):
     """The fp64 oracle eager recurrence, as it stands, on a bounded sample of the same
-    workload (all 64 x 32 heads, as many steps as fit the time budget)."""
+    workload shape (the B x H heads of one layer -- at most 64 x 32 x 128^2 -- for as
+    many steps as fit the time budget)."""
     from oracle import eager as OE
     from paper_2608_15533_amd import workloads as W
 
-    S = W.initial_state(w).astype(np.float64)
-    xs = [W.step_inputs(w, t) for t in range(4)]
+    B = w.B if w.B * w.H * w.dk * w.dv <= 64 * 32 * 128 * 128 else 64
+    ws = w.with_(B=B)
+    S = W.initial_state(ws).astype(np.float64)
+    xs = [W.step_inputs(ws, t) for t in range(4)]
+    u = W.bonus(ws)
+    u = None if u is None else np.broadcast_to(u, xs[0]["k"].shape)
     wall0, cpu0 = time.perf_counter(), time.process_time()
     steps = 0
     while True:
         x = xs[steps % len(xs)]
-        S, _ = OE.eager_step(w.op, S, x["q"], x["k"], x["v"], x["beta"], x["lam"])
+        S, _ = OE.eager_step(w.op, S, x["q"], x["k"], x["v"], x["beta"], x["lam"], u=u)
         steps += 1
         el = time.perf_counter() - wall0
         if el >= budget_s or steps >= 256:
             break
     cpu = time.process_time() - cpu0
     return {
-        "value": w.B * steps / el,
+        "value": round(B * steps / el, 2),
         "unit": "tokens/s",
         "cores": max(1, int(round(cpu / el))),
         "kind": "oracle",
-        "sample": f"fp64 eager oracle, {w.B}x{w.H} heads {w.dk}x{w.dv}, {steps} decode steps "
+        "sample": f"fp64 eager oracle, {B}x{w.H} heads of {w.dk}x{w.dv}, {steps} decode steps "
                   f"({el:.1f} s wall, {cpu:.1f} s CPU) on the host of this GPU",
     }
 
@@ -102,36 +158,54 @@ def main():
               "update has no cross-GPU step; run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
+    import ctypes
+
     import torch
     from paper_2608_15533_amd import deltalog as D
     from paper_2608_15533_amd import traffic as T
     from paper_2608_15533_amd import workloads as W
 
-    w = W.GDN_B64
-    R, K, WU = args.replicas, args.steps, args.warmup
+    w, R = workloads()[args.workload]
+    R = args.replicas or R
+    K, WU = args.steps, args.warmup
     dev = "cuda"
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
     sp = stream.cuda_stream
     desc = D.make_desc(w.op, w.B, w.H, w.dk, w.dv, w.M, w.in_dtype)
+    heads = w.B * w.H
+    it = torch.bfloat16 if w.in_dtype == "bf16" else torch.float32
 
     # -------------------------------------------------------------- device buffers
+    gen = torch.Generator(device=dev)
     states = []
     for r in range(R):
-        S0 = torch.from_numpy(W.initial_state(w, layer=r)).to(dev)
+        gen.manual_seed(20261202 + r)
+        S0 = torch.randn((w.B, w.H, w.dk, w.dv), generator=gen, device=dev) * 0.02
         states.append(D.DeltaLogState(desc, S0))
+        del S0
     eager_S = [s.S.clone() for s in states]
+    u = W.bonus(w)
     toks = []
     for t in range(POOL):
         x = W.step_inputs(w, t)
-        cv = lambda a, dt: torch.from_numpy(a).to(dev).to(dt).contiguous()
-        toks.append(D.Token(desc, w.B, cv(x["q"], torch.bfloat16), cv(x["k"], torch.bfloat16),
-                            cv(x["v"], torch.bfloat16), cv(x["lam"], torch.float32),
-                            cv(x["beta"], torch.float32)))
+        cv = lambda a, dt: None if a is None else torch.from_numpy(a).to(dev).to(dt).contiguous()
+        toks.append(D.Token(desc, w.B, cv(x["q"], it), cv(x["k"], it), cv(x["v"], it),
+                            cv(x["lam"], torch.float32), cv(x["beta"], torch.float32),
+                            cv(u, torch.float32)))
     outs = [torch.empty((w.B, w.H, w.dv), dtype=torch.float32, device=dev) for _ in range(R)]
+
+    # staggered log fill (partial-batch warm-up through slot lists)
+    live = np.zeros(w.B, dtype=np.int64)                 # host mirror of every slot's L
+    if w.staggered:
+        for rnd, rows in W.warmup_schedule(w):
+            sl = torch.from_numpy(rows.astype(np.int32)).to(dev)
+            for r in range(R):
+                D.dl_append_step(desc, states[r], toks[rnd % POOL], outs[r][: len(rows)], slots=sl)
+            live[rows] += 1
+        assert np.array_equal(live, W.fill_offsets(w))
     torch.cuda.synchronize()
 
-    import ctypes
     dref = ctypes.byref(desc)
     app = D.lib.dl_append_step
     eag = D.lib.dl_eager_step
@@ -141,18 +215,17 @@ def main():
                   outs[r].data_ptr(), None, w.B, sp) for t in range(POOL)] for r in range(R)]
 
     def run(fn, argtab, k0, nsteps, events=None):
+        i = 0
         for k in range(k0, k0 + nsteps):
             for r in range(R):
                 if events is not None:
-                    a = torch.cuda.Event(enable_timing=True)
-                    a.record(stream)
+                    events[i][0].record(stream)
                 rc = fn(*argtab[r][k % POOL])
                 if rc != 0:
                     raise D.DeltaLogError(rc, fn.__name__)
                 if events is not None:
-                    b = torch.cuda.Event(enable_timing=True)
-                    b.record(stream)
-                    events.append((a, b))
+                    events[i][1].record(stream)
+                i += 1
 
     def timed(fn, argtab):
         """W untimed steps, then K timed steps bracketed by synchronize + HIP events on
@@ -168,52 +241,70 @@ def main():
         return t0.elapsed_time(t1)
 
     def per_launch(fn, argtab, k0, nsteps):
-        """A separate pass with an event pair around every launch (per-phase split)."""
-        evs = []
+        """A separate pass with an event pair around every launch (per-phase split);
+        the events are created beforehand so the host keeps ahead of the device."""
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(nsteps * R)]
         run(fn, argtab, k0, nsteps, evs)
         torch.cuda.synchronize()
         return np.array([a.elapsed_time(b) for a, b in evs]).reshape(nsteps, R)
 
+    def launch_bytes(k):
+        """Algorithmic bytes of one layer launch at step k (every slot at its own L)."""
+        Ls = (live + k) % w.M
+        counts = np.bincount(Ls, minlength=w.M)
+        return sum(int(c) * w.H * T.step_bytes(w.op, w.dk, w.dv, w.M, L, w.in_dtype).total
+                   for L, c in enumerate(counts) if c)
+
     # ------------------------------------------------------------------ DeltaLog
     dl_ms = timed(app, app_args)
-    heads = w.B * w.H
-    Ls = [(WU + k) % w.M for k in range(K)]           # live length at each timed step
-    step_bytes = np.array([T.step_bytes(w.op, w.dk, w.dv, w.M, L, w.in_dtype).total * heads
-                           for L in Ls])
     n_launch = K * R
-    dl_tok = w.B * R * K / (dl_ms * 1e-3)
+    tokens = w.B * K if w.layers > 1 else w.B * R * K    # stack: tokens through all layers
+    dl_tok = tokens / (dl_ms * 1e-3)
     avg_launch_us = dl_ms * 1e3 / n_launch
-    bytes_per_launch = float(step_bytes.mean())
+    bytes_per_launch = float(np.mean([launch_bytes(WU + k) for k in range(K)]))
     achieved = bytes_per_launch / (avg_launch_us * 1e-6) / 1e9
 
-    # per-phase split: one more full cycle per replica, every launch bracketed
     k0 = WU + K
     PH = 2 * w.M
     ph_durs = per_launch(app, app_args, k0, PH)
     for s in states:
         assert int(s.err.item()) == 0
-    phases = {}
-    for L in range(w.M):
-        sel = np.array([(k0 + k) % w.M == L for k in range(PH)])
-        us = float(ph_durs[sel].mean() * 1e3)
-        b = T.step_bytes(w.op, w.dk, w.dv, w.M, L, w.in_dtype).total * heads
-        name = "merge_L%d" % L if L == w.M - 1 else f"append_L{L}"
-        phases[name] = {"us": round(us, 2), "GB/s": round(b / (us * 1e-6) / 1e9, 1)}
-    app_sel = np.array([(k0 + k) % w.M < w.M - 1 for k in range(PH)])
-    app_us = float(ph_durs[app_sel].mean() * 1e3)
-    app_bytes = float(np.mean([T.step_bytes(w.op, w.dk, w.dv, w.M, (k0 + k) % w.M, w.in_dtype).total
-                               for k in range(PH) if app_sel[k]]) * heads)
-    mrg_us = float(ph_durs[~app_sel].mean() * 1e3)
-    mrg_bytes = T.merge_bytes(w.op, w.dk, w.dv, w.M - 1, w.in_dtype).total * heads
+    phases = {"source": "separate pass, HIP event pair around each launch, median per phase"}
+    if not w.staggered:
+        by_L = {}
+        for L in range(w.M):
+            sel = np.array([(k0 + k) % w.M == L for k in range(PH)])
+            us = float(np.median(ph_durs[sel]) * 1e3)
+            b = T.step_bytes(w.op, w.dk, w.dv, w.M, L, w.in_dtype).total * heads
+            by_L[("merge_L%d" if L == w.M - 1 else "append_L%d") % L] = {
+                "us": round(us, 2), "GB/s": round(b / (us * 1e-6) / 1e9, 1)}
+        app_sel = np.array([(k0 + k) % w.M < w.M - 1 for k in range(PH)])
+        app_us = float(np.median(ph_durs[app_sel]) * 1e3)
+        app_b = float(np.mean([launch_bytes(k0 + k) for k in range(PH) if app_sel[k]]))
+        mrg_us = float(np.median(ph_durs[~app_sel]) * 1e3)
+        mrg_b = T.merge_bytes(w.op, w.dk, w.dv, w.M - 1, w.in_dtype).total * heads
+        for name, us, b in (("append", app_us, app_b), ("merge", mrg_us, mrg_b)):
+            gbs = b / (us * 1e-6) / 1e9
+            phases[name] = {"us": round(us, 2), "GB/s": round(gbs, 1),
+                            "frac": round(gbs / HBM_PEAK_GBS, 4)}
+        phases["by_live_length"] = by_L
+    else:
+        us = float(np.median(ph_durs) * 1e3)
+        b = float(np.mean([launch_bytes(k0 + k) for k in range(PH)]))
+        phases["mixed"] = {"us": round(us, 2), "GB/s": round(b / (us * 1e-6) / 1e9, 1),
+                           "note": "every launch mixes appending and merging slots"}
 
     # ------------------------------------------------------------------ eager baseline
     eg_ms = timed(eag, eag_args)
-    eg_tok = w.B * R * K / (eg_ms * 1e-3)
+    eg_tok = tokens / (eg_ms * 1e-3)
     eg_bytes = T.eager_bytes(w.op, w.dk, w.dv, w.in_dtype).total * heads
     eg_us = eg_ms * 1e3 / n_launch
     eg_gbs = eg_bytes / (eg_us * 1e-6) / 1e9
 
-    state_mib = w.B * w.H * w.dk * w.dv * 4 / 2**20
+    traffic, traffic_src = counter_traffic(args.workload)
+    state_mib = heads * w.dk * w.dv * 4 / 2**20
+    kname = {"gdn": "GDN", "kda": "KDA", "rwkv6": "RWKV6"}[w.op]
     res = {
         "metric": METRIC,
         "value": round(dl_tok, 1),
@@ -228,35 +319,35 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {
-            "workload": "GDN decode state update: B=64 sequences, H=32 heads, dk=dv=128, "
-                        "fp32 state, bf16 q/k/v, merge interval M=16",
-            "op": w.op, "batch": w.B, "heads": w.H, "dk": w.dk, "dv": w.dv,
-            "merge_interval": w.M, "in_dtype": w.in_dtype, "state_dtype": "f32",
-            "layer_replicas": R, "state_MiB_per_layer": state_mib,
+            "workload": (f"{kname} decode state update: B={w.B} sequences, H={w.H} heads, "
+                         f"dk={w.dk}, dv={w.dv}, fp32 state, {w.in_dtype} q/k/v, merge interval "
+                         f"M={w.M}" + (f", {w.layers} layers, staggered log fill"
+                                       if w.layers > 1 else "")),
+            "name": args.workload, "op": w.op, "batch": w.B, "heads": w.H, "dk": w.dk,
+            "dv": w.dv, "merge_interval": w.M, "in_dtype": w.in_dtype, "state_dtype": "f32",
+            "layer_states": R, "state_MiB_per_layer": state_mib,
             "working_set_MiB": round(sum(t.numel() * t.element_size() for st in states
                                          for t in st.buffers().values()) / 2**20, 1),
-            "tokens_per_s_definition": "per-layer token-updates/s = B*R*K/elapsed",
+            "tokens_per_s_definition": ("per-layer token-updates/s = B*R*K/elapsed"
+                                        if w.layers == 1 else
+                                        "tokens through all layers = B*K/elapsed"),
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": "deltalog_kernel<GDN,128,128,STEP,bf16> (dl_append_step: append or merge)",
+            "kernel": f"deltalog_kernel<{kname},{w.dk},{w.dv},STEP,{w.in_dtype}> "
+                      "(dl_append_step: append or merge)",
             "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": None,
+            "traffic": None if traffic is None else round(traffic, 1),
+            "traffic_unit": "bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
+            "traffic_source": traffic_src,
             "avg_launch_us": round(avg_launch_us, 3),
             "algorithmic_bytes_per_launch": round(bytes_per_launch, 1),
             "duration_source": "HIP events around the timed region / launches",
         },
-        "phases": {
-            "source": "separate pass, HIP event pair around each launch",
-            "append": {"us": round(app_us, 2), "GB/s": round(app_bytes / (app_us * 1e-6) / 1e9, 1),
-                       "frac": round(app_bytes / (app_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)},
-            "merge": {"us": round(mrg_us, 2), "GB/s": round(mrg_bytes / (mrg_us * 1e-6) / 1e9, 1),
-                      "frac": round(mrg_bytes / (mrg_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)},
-            "by_live_length": phases,
-        },
+        "phases": phases,
         "eager": {
             "tokens_per_s": round(eg_tok, 1),
             "ms_per_step": round(eg_ms / K, 5),
@@ -266,6 +357,7 @@ def main():
         },
         "speedup_vs_eager": round(dl_tok / eg_tok, 3),
         "state_write_ratio_model": round(T.state_write_ratio(w.op, w.dk, w.dv, w.M, w.in_dtype), 2),
+        "kernel_source_hash": kernel_source_hash(),
     }
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
