@@ -2,9 +2,9 @@
 //
 // One workgroup owns one (slot, head) state: a dk x dv fp32 matrix (64 KiB at 128x128).
 // Thread layout: NCG = dv/4 column groups (one float4 column slice each) times
-// NRG = dk/16 row groups; every thread keeps 16 rows x 4 columns of the state in
+// NRG = dk/RPT row groups; every thread keeps RPT rows x 4 columns of the state in
 // registers (rows rg, rg+NRG, ..., so one wave-wide float4 load covers whole
-// consecutive rows, 1 KiB contiguous).  The state is read from HBM exactly once
+// consecutive rows, 1 KiB contiguous).  RPT = 16, or 8 for 64 x 64 heads.  The state is read from HBM exactly once
 // per step and, when the step materialises (merge / eager / flush), written back
 // exactly once from the same registers -- the read, the key-dimension reductions
 // and the write never leave the workgroup.  Because one workgroup owns all of a
@@ -96,6 +96,9 @@ __device__ __forceinline__ float shfl_xor(float v, int m) { return __shfl_xor(v,
 #ifndef DL_PREFETCH_PER_KEY
 #define DL_PREFETCH_PER_KEY 0
 #endif
+#ifndef DL_PREFETCH_PER_KEY_SMALL
+#define DL_PREFETCH_PER_KEY_SMALL 0
+#endif
 // Occupancy target (waves per SIMD) handed to the register allocator; 0 = compiler's choice.
 #ifndef DL_WAVES_PER_EU
 #define DL_WAVES_PER_EU 0
@@ -150,9 +153,20 @@ __device__ __forceinline__ void ld_run(const uint16_t* p, float (&o)[N]) {
 constexpr uint32_t kXcds = 8;   // accelerator complex dies of an MI355X
 
 // ------------------------------------------------------------------ configuration
+// Threads per workgroup for a dk x dv head: dv/4 column groups x dk/rows-per-thread
+// row groups.  Small (64 x 64) heads keep 8 rows per thread (two waves per head), the
+// others 16 rows per thread.
+#ifndef DL_SMALL_HEAD_RPT
+#define DL_SMALL_HEAD_RPT 8
+#endif
+constexpr int rows_per_thread(int dk, int dv) {
+  return (dk == 64 && dv == 64) ? DL_SMALL_HEAD_RPT : 16;
+}
+constexpr int threads_per_head(int dk, int dv) { return (dv / 4) * (dk / rows_per_thread(dk, dv)); }
+
 template <int OP, int DK, int DV, int MODE>
 struct Cfg {
-  static constexpr int RPT = 16;                 // state rows held per thread
+  static constexpr int RPT = rows_per_thread(DK, DV);   // state rows held per thread
   static constexpr int NCG = DV / 4;             // float4 column groups
   static constexpr int NRG = DK / RPT;           // row groups
   static constexpr int NT = NCG * NRG;           // threads per workgroup
@@ -178,7 +192,7 @@ struct Cfg {
   static_assert(RPL == 8 || RPL == 16, "coefficient pass run length");
   static_assert(CH == EPP, "the first merge chunk is staged by the first coefficient pass");
   static_assert(LPE <= 64 && 64 % LPE == 0, "an entry's lanes share one wave");
-  static_assert(NT == (DV / 4) * (DK / 16), "launch bound must match the layout");
+  static_assert(NT == threads_per_head(DK, DV), "launch bound must match the layout");
 };
 
 template <int OP, typename TIN>
@@ -197,7 +211,7 @@ struct UType<OP_RWKV6, TIN> { using type = TIN; };  // RWKV6: U_log holds exact 
 // tile, the token rows, the first pass of log keys/snapshots and the first log values
 // of the replay; only the live length (and the slot id, for slot lists) precede them.
 template <int OP, int DK, int DV, int MODE, typename TIN>
-__global__ __launch_bounds__((DV / 4) * (DK / 16)) DL_OCCUPANCY
+__global__ __launch_bounds__(threads_per_head(DK, DV)) DL_OCCUPANCY
 void deltalog_kernel(KParams p) {
   using CF = Cfg<OP, DK, DV, MODE>;
   using TU = typename UType<OP, TIN>::type;
@@ -290,8 +304,10 @@ void deltalog_kernel(KParams p) {
   const TU* Ub = static_cast<const TU*>(p.u_log) + sh * size_t(C) * DV;
   const int e_ = tid / CF::LPE;                   // coefficient pass: entry within the pass
   const int c_ = tid % CF::LPE;                   //                   key-row run
+  // Per-key snapshots are prefetched only where the registers allow it (small heads).
+  constexpr bool kPrefetchPerKey = DL_PREFETCH_PER_KEY || (DL_PREFETCH_PER_KEY_SMALL && RPT == 8);
   float kr[RPL], lr_[(DL == 1) ? 1 : RPL];
-  if constexpr (CF::REPLAYS && DL_PREFETCH_KEYS && (DL == 1 || DL_PREFETCH_PER_KEY)) {
+  if constexpr (CF::REPLAYS && DL_PREFETCH_KEYS && (DL == 1 || kPrefetchPerKey)) {
     if (e_ < L) {
       ld_run<RPL>(Kb + size_t(e_) * DK + c_ * RPL, kr);
       if constexpr (DL == 1) lr_[0] = Lb[e_];
@@ -358,7 +374,7 @@ void deltalog_kernel(KParams p) {
       const bool stage = CF::MERGES_LOG && merging && i0 == 0;
       float ak = 0.f, aq = 0.f;
       if (i < L) {
-        if (i0 > 0 || !DL_PREFETCH_KEYS || (DL != 1 && !DL_PREFETCH_PER_KEY)) {
+        if (i0 > 0 || !DL_PREFETCH_KEYS || (DL != 1 && !kPrefetchPerKey)) {
           ld_run<RPL>(Kb + size_t(i) * DK + c_ * RPL, kr);
           if constexpr (DL == 1) lr_[0] = Lb[i];
           else ld_run<RPL>(Lb + size_t(i) * DK + c_ * RPL, lr_);
