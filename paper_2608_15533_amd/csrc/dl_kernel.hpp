@@ -78,6 +78,12 @@ __device__ __forceinline__ float4 fma4(float s, float4 b, float4 a) {
 
 __device__ __forceinline__ float shfl_xor(float v, int m) { return __shfl_xor(v, m, 64); }
 
+// Decay factors exp(x) for log-decay differences x <= 0: the hardware base-2
+// exponential of x * log2(e) (two instructions instead of the 13 of a correctly
+// rounded expf).  Its relative error is about 2^-24 * |x| * log2(e) plus one ulp
+// (below 2e-6 for |x| <= 40); exp(0) is exactly 1.
+__device__ __forceinline__ float dl_exp(float x) { return __expf(x); }
+
 // State-tile traffic.  The base is streamed once per step and not reused by this
 // workgroup, so by default its loads and stores carry the non-temporal hint.
 #ifndef DL_NT_STATE
@@ -97,7 +103,11 @@ __device__ __forceinline__ float shfl_xor(float v, int m) { return __shfl_xor(v,
 #define DL_PREFETCH_PER_KEY 0
 #endif
 #ifndef DL_PREFETCH_PER_KEY_SMALL
-#define DL_PREFETCH_PER_KEY_SMALL 0
+#define DL_PREFETCH_PER_KEY_SMALL 1
+#endif
+// Issue order of the log entries relative to the state tile (see the kernel).
+#ifndef DL_LOG_FIRST
+#define DL_LOG_FIRST 0
 #endif
 // Occupancy target (waves per SIMD) handed to the register allocator; 0 = compiler's choice.
 #ifndef DL_WAVES_PER_EU
@@ -151,6 +161,60 @@ __device__ __forceinline__ void ld_run(const uint16_t* p, float (&o)[N]) {
 }
 
 constexpr uint32_t kXcds = 8;   // accelerator complex dies of an MI355X
+
+// Raw register images of loads whose conversion to fp32 is deferred: converting right
+// after a load makes the wave wait for it, and (loads completing in issue order) for
+// every load issued before it -- the state tile included.
+__device__ __forceinline__ float to_f32(float x) { return x; }
+__device__ __forceinline__ float to_f32(uint16_t x) { return __uint_as_float(uint32_t(x) << 16); }
+
+template <typename T> struct Raw4;                 // four consecutive elements
+template <> struct Raw4<float> {
+  float4 w;
+  __device__ __forceinline__ void load(const float* p) { w = *reinterpret_cast<const float4*>(p); }
+  __device__ __forceinline__ float4 get() const { return w; }
+};
+template <> struct Raw4<uint16_t> {
+  uint2 w;
+  __device__ __forceinline__ void load(const uint16_t* p) { w = *reinterpret_cast<const uint2*>(p); }
+  __device__ __forceinline__ float4 get() const {
+    return make_float4(bf_lo(w.x), bf_hi(w.x), bf_lo(w.y), bf_hi(w.y));
+  }
+};
+
+template <typename T, int N> struct RawRun;         // N consecutive elements, N % 8 == 0
+template <int N> struct RawRun<float, N> {
+  float4 w[N / 4];
+  __device__ __forceinline__ void load(const float* p) {
+#pragma unroll
+    for (int i = 0; i < N / 4; ++i) w[i] = reinterpret_cast<const float4*>(p)[i];
+  }
+  __device__ __forceinline__ void get(float (&o)[N]) const {
+#pragma unroll
+    for (int i = 0; i < N / 4; ++i) {
+      o[4 * i] = w[i].x; o[4 * i + 1] = w[i].y; o[4 * i + 2] = w[i].z; o[4 * i + 3] = w[i].w;
+    }
+  }
+};
+template <int N> struct RawRun<uint16_t, N> {
+  uint4 w[N / 8];
+  __device__ __forceinline__ void load(const uint16_t* p) {
+#pragma unroll
+    for (int i = 0; i < N / 8; ++i) w[i] = reinterpret_cast<const uint4*>(p)[i];
+  }
+  __device__ __forceinline__ void get(float (&o)[N]) const {
+#pragma unroll
+    for (int i = 0; i < N / 8; ++i) {
+      o[8 * i + 0] = bf_lo(w[i].x); o[8 * i + 1] = bf_hi(w[i].x);
+      o[8 * i + 2] = bf_lo(w[i].y); o[8 * i + 3] = bf_hi(w[i].y);
+      o[8 * i + 4] = bf_lo(w[i].z); o[8 * i + 5] = bf_hi(w[i].z);
+      o[8 * i + 6] = bf_lo(w[i].w); o[8 * i + 7] = bf_hi(w[i].w);
+    }
+  }
+};
+
+// Nothing may be scheduled across this point (loads keep their issue order).
+__device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
 
 // ------------------------------------------------------------------ configuration
 // Threads per workgroup for a dk x dv head: dv/4 column groups x dk/rows-per-thread
@@ -207,8 +271,8 @@ struct UType<OP_RWKV6, TIN> { using type = TIN; };  // RWKV6: U_log holds exact 
 #endif
 
 // ------------------------------------------------------------------ the kernel
-// Every global load a workgroup needs is issued before its first barrier: the state
-// tile, the token rows, the first pass of log keys/snapshots and the first log values
+// Every global load a workgroup needs is issued before its first barrier: the token
+// rows, the state tile, the first pass of log keys/snapshots and the first log values
 // of the replay; only the live length (and the slot id, for slot lists) precede them.
 template <int OP, int DK, int DV, int MODE, typename TIN>
 __global__ __launch_bounds__(threads_per_head(DK, DV)) DL_OCCUPANCY
@@ -257,18 +321,55 @@ void deltalog_kernel(KParams p) {
   int L_raw = 0;
   if constexpr (CF::HAS_LOG) L_raw = p.len[sh];
 
-  // ---- 1. the state tile (the dominant HBM stream) --------------------------------
+  // Vector loads return in issue order, so a wait for one load is a wait for every
+  // load issued before it.  The issue order is therefore: the small token rows (needed
+  // first, by the prologue), then the 64 KiB state tile, then the log entries (needed
+  // after the first barrier, once the live length is known).  Compiler barriers keep
+  // that order.
+
+  // ---- 1. token row values (the prologue's inputs) ---------------------------------
+  const TIN* kin = static_cast<const TIN*>(p.k) + th * DK;
+  const TIN* qin = static_cast<const TIN*>(p.q) + th * DK;
   const int cg = tid % NCG;
   const int rg = tid / NCG;
+  const int r0 = tid;                              // this thread's key row in the prologue
+  // Every thread loads (threads past dk re-read the last row and ignore it): a load
+  // under a branch would need its value at the branch join, i.e. an early wait.
+  const int rl = r0 < DK ? r0 : DK - 1;
+  const int rd = (DL == 1) ? 0 : rl;
+  TIN k_raw = TIN(0), q_raw = TIN(0);
+  float lam = 0.f, ell = 0.f, uf = 0.f;
+  if constexpr (CF::HAS_TOKEN) {
+    k_raw = kin[rl];
+    lam = p.lam[th * DL + rd];
+    if constexpr (!CF::DELTA) uf = p.u[size_t(h) * DK + rl];
+  }
+  if constexpr (CF::READS_OUT) q_raw = qin[rl];
+  if constexpr (CF::HAS_LOG) ell = p.ell[sh * DL + rd];
+  Raw4<TIN> v_raw{};
+  float beta = 0.f;
+  if constexpr (CF::HAS_TOKEN) {
+    v_raw.load(static_cast<const TIN*>(p.v) + th * DV + 4 * cg);
+    if constexpr (CF::DELTA) beta = p.beta[th];
+  }
+  asm volatile("" ::: "memory");
+  sched_fence();
+
+  // ---- 2. the state tile and the log entries of the first pass ---------------------
+  // Default order: tile, then (once the live length is back) the log entries, so the
+  // tile never waits for the length.  DL_LOG_FIRST = 1 waits for the length first and
+  // issues the log entries ahead of the tile, so the coefficient pass does not wait
+  // for the tile.
   const auto srs = state_rsrc(p.S + sh * size_t(DK) * DV, DK * DV * 4);
   const uint32_t toff = uint32_t(rg * DV + 4 * cg) * 4;   // this lane's byte offset in a row block
   constexpr uint32_t kRowBlock = NRG * DV * 4;             // bytes between row j and row j+1 of a lane
   float4 t[RPT];
+  if constexpr (!DL_LOG_FIRST) {
 #pragma unroll
-  for (int j = 0; j < RPT; ++j) t[j] = ld_state(srs, toff, j * kRowBlock);
-  // Keep every use of the live length (and the branches on it) behind the tile loads,
-  // so the tile is in flight while the length comes back.
-  asm volatile("" ::: "memory");
+    for (int j = 0; j < RPT; ++j) t[j] = ld_state(srs, toff, j * kRowBlock);
+    asm volatile("" ::: "memory");
+    sched_fence();
+  }
 
   int L = __builtin_amdgcn_readfirstlane(L_raw);
   const bool bad_len = L < 0 || L > C;
@@ -278,27 +379,6 @@ void deltalog_kernel(KParams p) {
     return;
   }
 
-  // ---- 2. register prefetch: token row values, log entries of the first pass -------
-  const TIN* kin = static_cast<const TIN*>(p.k) + th * DK;
-  const TIN* qin = static_cast<const TIN*>(p.q) + th * DK;
-  const int r0 = tid;                              // this thread's key row in the prologue
-  float kf = 0.f, qf = 0.f, lam = 0.f, ell = 0.f, uf = 0.f;
-  if (r0 < DK) {
-    const int rd = (DL == 1) ? 0 : r0;
-    if constexpr (CF::HAS_TOKEN) {
-      kf = ld1(kin + r0);
-      lam = p.lam[th * DL + rd];
-      if constexpr (!CF::DELTA) uf = p.u[size_t(h) * DK + r0];
-    }
-    if constexpr (CF::READS_OUT) qf = ld1(qin + r0);
-    if constexpr (CF::HAS_LOG) ell = p.ell[sh * DL + rd];
-  }
-  float4 vv = f4(0.f);
-  float beta = 0.f;
-  if constexpr (CF::HAS_TOKEN) {
-    vv = ld4(static_cast<const TIN*>(p.v) + th * DV + 4 * cg);
-    if constexpr (CF::DELTA) beta = p.beta[th];
-  }
   const TIN* Kb = static_cast<const TIN*>(p.k_log) + sh * size_t(C) * DK;
   const float* Lb = p.lam_log + sh * size_t(C) * DL;
   const TU* Ub = static_cast<const TU*>(p.u_log) + sh * size_t(C) * DV;
@@ -307,18 +387,35 @@ void deltalog_kernel(KParams p) {
   // Per-key snapshots are prefetched only where the registers allow it (small heads).
   constexpr bool kPrefetchPerKey = DL_PREFETCH_PER_KEY || (DL_PREFETCH_PER_KEY_SMALL && RPT == 8);
   float kr[RPL], lr_[(DL == 1) ? 1 : RPL];
+  RawRun<TIN, RPL> kr_raw{};
+  RawRun<float, (DL == 1) ? 8 : RPL> lr_raw{};      // per-key snapshots (unused for DL == 1)
+  float lr0 = 0.f;                                   // scalar snapshot (DL == 1)
+  // The prefetch loads are unconditional (a load under a per-lane condition makes the
+  // wait counters conservative, i.e. waits for the tile): lanes past the live length
+  // re-read entry L-1 (same cache lines), an empty log reads entry 0, and a log of
+  // capacity 0 reads the head's own state tile instead; such values are never used.
+  const int Lm1 = L > 0 ? L - 1 : 0;
+  const TIN* Kp = C > 0 ? Kb : reinterpret_cast<const TIN*>(p.S + sh * size_t(DK) * DV);
+  const float* Lp = C > 0 ? Lb : p.S + sh * size_t(DK) * DV;
+  const TU* Up = C > 0 ? Ub : reinterpret_cast<const TU*>(p.S + sh * size_t(DK) * DV);
   if constexpr (CF::REPLAYS && DL_PREFETCH_KEYS && (DL == 1 || kPrefetchPerKey)) {
-    if (e_ < L) {
-      ld_run<RPL>(Kb + size_t(e_) * DK + c_ * RPL, kr);
-      if constexpr (DL == 1) lr_[0] = Lb[e_];
-      else ld_run<RPL>(Lb + size_t(e_) * DK + c_ * RPL, lr_);
-    }
+    const int ek = min(e_, Lm1);
+    kr_raw.load(Kp + size_t(ek) * DK + c_ * RPL);
+    if constexpr (DL == 1) lr0 = Lp[ek];
+    else lr_raw.load(Lp + size_t(ek) * DK + c_ * RPL);
   }
-  float4 up0 = f4(0.f), up1 = f4(0.f);            // first two replay values of this row group
+  Raw4<TU> up0_raw{}, up1_raw{};                     // first two replay values of this row group
   if constexpr (CF::REPLAYS && DL_PREFETCH_U) {
-    if (rg < L) up0 = ld4(Ub + size_t(rg) * DV + 4 * cg);
-    if (rg + NRG < L) up1 = ld4(Ub + size_t(rg + NRG) * DV + 4 * cg);
+    up0_raw.load(Up + size_t(min(rg, Lm1)) * DV + 4 * cg);
+    up1_raw.load(Up + size_t(min(rg + NRG, Lm1)) * DV + 4 * cg);
   }
+  if constexpr (DL_LOG_FIRST) {
+    sched_fence();
+#pragma unroll
+    for (int j = 0; j < RPT; ++j) t[j] = ld_state(srs, toff, j * kRowBlock);
+  }
+  sched_fence();
+  const float kf = to_f32(k_raw), qf = to_f32(q_raw);
 
   // Does this (slot, head) materialise in this launch?  (Uniform per workgroup.)
   const bool merging = MODE == M_MERGE || MODE == M_FLUSH || MODE == M_EAGER ||
@@ -331,7 +428,7 @@ void deltalog_kernel(KParams p) {
         if (x / NCG >= L) s_u[x] = f4(0.f);
   }
 
-  // ---- 3. per-row decay factors (LDS) and the token dot product ---------------------
+  // ---- 4. per-row decay factors (LDS) and the token dot product ---------------------
   if (r0 < DK) {
     float lr, lm;
     if constexpr (MODE == M_EAGER) {
@@ -344,12 +441,12 @@ void deltalog_kernel(KParams p) {
       lr = ell;
       lm = ell;
     }
-    const float er = expf(lr);
+    const float er = dl_exp(lr);
     s_kf[r0] = kf;
     s_qf[r0] = qf;
     s_xk[r0] = er * kf;
     s_xq[r0] = er * qf;
-    s_em[r0] = expf(lm);
+    s_em[r0] = dl_exp(lm);
     if (r0 < DL) {
       s_lr[r0] = lr;
       s_lm[r0] = lm;
@@ -358,13 +455,14 @@ void deltalog_kernel(KParams p) {
   if constexpr (CF::HAS_TOKEN) {
     // q.k (delta rule, post-update readout) or r.(u*k) (RWKV6 bonus)
     float d = CF::DELTA ? qf * kf : qf * uf * kf;
+    if (r0 >= DK) d = 0.f;                        // threads past dk hold a repeated row
 #pragma unroll
     for (int m = 32; m >= 1; m >>= 1) d += shfl_xor(d, m);
     if ((tid & 63) == 0) s_dotw[tid >> 6] = d;
   }
   __syncthreads();
 
-  // ---- 4. replay coefficients g_i(k), g_i(q) of the live entries --------------------
+  // ---- 5. replay coefficients g_i(k), g_i(q) of the live entries --------------------
   // A merging workgroup also writes the first chunk of decayed keys
   // K~_i[r] = e^(l'_r - Lam_i,r) K_i[r] to LDS here, from the same loads (for the delta
   // rule the merge decay l' equals the readout decay; RWKV6 reads at ell, merges at l').
@@ -378,6 +476,10 @@ void deltalog_kernel(KParams p) {
           ld_run<RPL>(Kb + size_t(i) * DK + c_ * RPL, kr);
           if constexpr (DL == 1) lr_[0] = Lb[i];
           else ld_run<RPL>(Lb + size_t(i) * DK + c_ * RPL, lr_);
+        } else {
+          kr_raw.get(kr);
+          if constexpr (DL == 1) lr_[0] = lr0;
+          else lr_raw.get(lr_);
         }
         if constexpr (DL == 1) {
 #pragma unroll
@@ -386,7 +488,7 @@ void deltalog_kernel(KParams p) {
             ak = fmaf(kr[x], s_kf[r], ak);
             aq = fmaf(kr[x], s_qf[r], aq);
           }
-          const float w = expf(s_lr[0] - lr_[0]);
+          const float w = dl_exp(s_lr[0] - lr_[0]);
           ak *= w;
           aq *= w;
           if (stage) {
@@ -397,10 +499,10 @@ void deltalog_kernel(KParams p) {
 #pragma unroll 2
           for (int x = 0; x < RPL; ++x) {
             const int r = c_ * RPL + x;
-            const float wk = expf(s_lr[r] - lr_[x]) * kr[x];
+            const float wk = dl_exp(s_lr[r] - lr_[x]) * kr[x];
             ak = fmaf(wk, s_kf[r], ak);
             aq = fmaf(wk, s_qf[r], aq);
-            if (stage) s_kt[r * CF::KTS + e_] = CF::DELTA ? wk : expf(s_lm[r] - lr_[x]) * kr[x];
+            if (stage) s_kt[r * CF::KTS + e_] = CF::DELTA ? wk : dl_exp(s_lm[r] - lr_[x]) * kr[x];
           }
         }
       } else if (stage) {
@@ -420,7 +522,7 @@ void deltalog_kernel(KParams p) {
     __syncthreads();
   }
 
-  // ---- 5. base readouts from the registers + log replay, reduced over rows -------
+  // ---- 6. base readouts from the registers + log replay, reduced over rows -------
   float4 cv = f4(0.f), ov = f4(0.f);
   if constexpr (CF::READS_OUT) {
 #pragma unroll
@@ -433,6 +535,7 @@ void deltalog_kernel(KParams p) {
       // Each log value row is read by exactly one row group; a merging workgroup keeps
       // the first chunk of them in LDS for the merge contraction.
       const bool stage_u = CF::MERGES_LOG && merging;
+      const float4 up0 = up0_raw.get(), up1 = up1_raw.get();
       if (DL_PREFETCH_U && rg < L) {
         if constexpr (CF::NEEDS_C) cv = fma4(s_gk[rg], up0, cv);
         ov = fma4(s_gq[rg], up0, ov);
@@ -477,9 +580,10 @@ void deltalog_kernel(KParams p) {
     }
   }
 
-  // ---- 6. update factors and output ------------------------------------------------
+  // ---- 7. update factors and output ------------------------------------------------
   float4 bv = f4(0.f);
   if constexpr (CF::HAS_TOKEN) {
+    const float4 vv = v_raw.get();
     float dot = 0.f;
 #pragma unroll
     for (int w2 = 0; w2 < CF::NW; ++w2) dot += s_dotw[w2];
@@ -496,7 +600,7 @@ void deltalog_kernel(KParams p) {
   }
   if constexpr (MODE == M_READOUT) return;
 
-  // ---- 7a. append (Eq. 5): L < C in STEP mode --------------------------------------
+  // ---- 8a. append (Eq. 5): L < C in STEP mode --------------------------------------
   if constexpr (MODE == M_STEP) {
     if (L < C) {
       const size_t ent = sh * size_t(C) + L;
@@ -518,7 +622,7 @@ void deltalog_kernel(KParams p) {
     }
   }
 
-  // ---- 7b. materialise (Eq. 6 / Eq. 7 / Eq. 3) ---------------------------------------
+  // ---- 8b. materialise (Eq. 6 / Eq. 7 / Eq. 3) ---------------------------------------
   if constexpr (CF::CAN_MERGE) {
 #pragma unroll
     for (int j = 0; j < RPT; ++j) {
@@ -538,7 +642,7 @@ void deltalog_kernel(KParams p) {
           if (ii < n) {
             const int i = i0 + ii;
             const float lam_i = Lb[size_t(i) * DL + ((DL == 1) ? 0 : r)];
-            val = expf(s_lm[(DL == 1) ? 0 : r] - lam_i) * ld1(Kb + size_t(i) * DK + r);
+            val = dl_exp(s_lm[(DL == 1) ? 0 : r] - lam_i) * ld1(Kb + size_t(i) * DK + r);
           }
           s_kt[r * CF::KTS + ii] = val;             // K~_i[r] = e^(l'_r - Lam_i,r) K_i[r]
         }
