@@ -64,6 +64,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=256)
     ap.add_argument("--warmup", type=int, default=32)
     ap.add_argument("--replicas", type=int, default=0, help="layer states (0: workload default)")
+    ap.add_argument("--state-dtype", default="f32", choices=("f32", "bf16"),
+                    help="dtype of the dense state (bf16: rounded on every store)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -100,10 +102,14 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
-def counter_traffic(workload):
+def profile_key(workload, state_dtype):
+    return workload + ("_bf16state" if state_dtype == "bf16" else "")
+
+
+def counter_traffic(key):
     """HBM bytes per launch of the dominant kernel from the committed counter profile,
     or None when there is none or the kernel sources changed since it was taken."""
-    path = os.path.join(ROOT, "profiles", f"{workload}_hbm_counters.txt")
+    path = os.path.join(ROOT, "profiles", f"{key}_hbm_counters.txt")
     if not os.path.exists(path):
         return None, "no counter profile"
     m = re.search(r"^TRAFFIC_JSON (\{.*\})$", open(path).read(), flags=re.M)
@@ -172,7 +178,8 @@ def main():
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
     sp = stream.cuda_stream
-    desc = D.make_desc(w.op, w.B, w.H, w.dk, w.dv, w.M, w.in_dtype)
+    sd = args.state_dtype
+    desc = D.make_desc(w.op, w.B, w.H, w.dk, w.dv, w.M, w.in_dtype, sd)
     heads = w.B * w.H
     it = torch.bfloat16 if w.in_dtype == "bf16" else torch.float32
 
@@ -253,7 +260,7 @@ def main():
         """Algorithmic bytes of one layer launch at step k (every slot at its own L)."""
         Ls = (live + k) % w.M
         counts = np.bincount(Ls, minlength=w.M)
-        return sum(int(c) * w.H * T.step_bytes(w.op, w.dk, w.dv, w.M, L, w.in_dtype).total
+        return sum(int(c) * w.H * T.step_bytes(w.op, w.dk, w.dv, w.M, L, w.in_dtype, sd).total
                    for L, c in enumerate(counts) if c)
 
     # ------------------------------------------------------------------ DeltaLog
@@ -276,14 +283,14 @@ def main():
         for L in range(w.M):
             sel = np.array([(k0 + k) % w.M == L for k in range(PH)])
             us = float(np.median(ph_durs[sel]) * 1e3)
-            b = T.step_bytes(w.op, w.dk, w.dv, w.M, L, w.in_dtype).total * heads
+            b = T.step_bytes(w.op, w.dk, w.dv, w.M, L, w.in_dtype, sd).total * heads
             by_L[("merge_L%d" if L == w.M - 1 else "append_L%d") % L] = {
                 "us": round(us, 2), "GB/s": round(b / (us * 1e-6) / 1e9, 1)}
         app_sel = np.array([(k0 + k) % w.M < w.M - 1 for k in range(PH)])
         app_us = float(np.median(ph_durs[app_sel]) * 1e3)
         app_b = float(np.mean([launch_bytes(k0 + k) for k in range(PH) if app_sel[k]]))
         mrg_us = float(np.median(ph_durs[~app_sel]) * 1e3)
-        mrg_b = T.merge_bytes(w.op, w.dk, w.dv, w.M - 1, w.in_dtype).total * heads
+        mrg_b = T.merge_bytes(w.op, w.dk, w.dv, w.M - 1, w.in_dtype, sd).total * heads
         for name, us, b in (("append", app_us, app_b), ("merge", mrg_us, mrg_b)):
             gbs = b / (us * 1e-6) / 1e9
             phases[name] = {"us": round(us, 2), "GB/s": round(gbs, 1),
@@ -298,12 +305,12 @@ def main():
     # ------------------------------------------------------------------ eager baseline
     eg_ms = timed(eag, eag_args)
     eg_tok = tokens / (eg_ms * 1e-3)
-    eg_bytes = T.eager_bytes(w.op, w.dk, w.dv, w.in_dtype).total * heads
+    eg_bytes = T.eager_bytes(w.op, w.dk, w.dv, w.in_dtype, sd).total * heads
     eg_us = eg_ms * 1e3 / n_launch
     eg_gbs = eg_bytes / (eg_us * 1e-6) / 1e9
 
-    traffic, traffic_src = counter_traffic(args.workload)
-    state_mib = heads * w.dk * w.dv * 4 / 2**20
+    traffic, traffic_src = counter_traffic(profile_key(args.workload, sd))
+    state_mib = heads * w.dk * w.dv * (2 if sd == "bf16" else 4) / 2**20
     kname = {"gdn": "GDN", "kda": "KDA", "rwkv6": "RWKV6"}[w.op]
     res = {
         "metric": METRIC,
@@ -320,11 +327,12 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": (f"{kname} decode state update: B={w.B} sequences, H={w.H} heads, "
-                         f"dk={w.dk}, dv={w.dv}, fp32 state, {w.in_dtype} q/k/v, merge interval "
+                         f"dk={w.dk}, dv={w.dv}, {'fp32' if sd == 'f32' else 'bf16'} state, "
+                         f"{w.in_dtype} q/k/v, merge interval "
                          f"M={w.M}" + (f", {w.layers} layers, staggered log fill"
                                        if w.layers > 1 else "")),
             "name": args.workload, "op": w.op, "batch": w.B, "heads": w.H, "dk": w.dk,
-            "dv": w.dv, "merge_interval": w.M, "in_dtype": w.in_dtype, "state_dtype": "f32",
+            "dv": w.dv, "merge_interval": w.M, "in_dtype": w.in_dtype, "state_dtype": sd,
             "layer_states": R, "state_MiB_per_layer": state_mib,
             "working_set_MiB": round(sum(t.numel() * t.element_size() for st in states
                                          for t in st.buffers().values()) / 2**20, 1),
@@ -334,7 +342,7 @@ def main():
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": f"deltalog_kernel<{kname},{w.dk},{w.dv},STEP,{w.in_dtype}> "
+            "kernel": f"deltalog_kernel<{kname},{w.dk},{w.dv},STEP,{w.in_dtype},{sd} state> "
                       "(dl_append_step: append or merge)",
             "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBS,
@@ -356,7 +364,7 @@ def main():
             "frac": round(eg_gbs / HBM_PEAK_GBS, 4),
         },
         "speedup_vs_eager": round(dl_tok / eg_tok, 3),
-        "state_write_ratio_model": round(T.state_write_ratio(w.op, w.dk, w.dv, w.M, w.in_dtype), 2),
+        "state_write_ratio_model": round(T.state_write_ratio(w.op, w.dk, w.dv, w.M, w.in_dtype, sd), 2),
         "kernel_source_hash": kernel_source_hash(),
     }
     if not args.no_cpu_baseline:

@@ -52,7 +52,7 @@
 extern "C" {
 #endif
 
-#define DL_ABI_VERSION 1
+#define DL_ABI_VERSION 2
 #define DL_MAX_MERGE_INTERVAL 64
 
 typedef enum {
@@ -84,11 +84,14 @@ typedef struct {
   int32_t in_dtype;       /* dl_dtype of q/r, k, v; K_log stores exact copies of k       */
   int32_t u_log_dtype;    /* dl_dtype of U_log: DL_F32 for GDN/KDA (corrected values),   */
                           /* == in_dtype for RWKV6 (exact copies of v)                   */
+  int32_t state_dtype;    /* dl_dtype of the dense state S: DL_F32, or DL_BF16 (all       */
+                          /* arithmetic in fp32, S rounded to bf16 -- nearest even -- on  */
+                          /* every store; every other buffer keeps its dtype)            */
 } dl_desc;
 
 /* DeltaLog physical state (Sec. 3.1 list of buffers), one entry per (slot, head). */
 typedef struct {
-  float*   S;        /* [B,H,dk,dv] fp32 dense base                                      */
+  void*    S;        /* [B,H,dk,dv] state_dtype dense base                               */
   float*   ell;      /* [B,H,dl]    fp32 cumulative log-decay since the last merge       */
   void*    k_log;    /* [B,H,C,dk]  in_dtype   key-side factors   (may be NULL if C == 0) */
   void*    u_log;    /* [B,H,C,dv]  u_log_dtype value-side factors (may be NULL if C == 0)*/
@@ -108,10 +111,11 @@ typedef struct {
 } dl_token;
 
 /* Eager dense step (Eq. 3): S <- D(lambda) S + a b^T with the readout of Table 1, for
- * the listed slots of a dense state S [B,H,dk,dv] fp32 (no log).  Writes o [n,H,dv].
+ * the listed slots of a dense state S [B,H,dk,dv] of state_dtype (no log).  Writes
+ * o [n,H,dv].
  * This is the baseline that reads and writes the whole state every token (Sec. 2.3).
  * desc->merge_interval is validated but otherwise ignored. */
-int dl_eager_step(const dl_desc* desc, float* S, const dl_token* tok, float* o,
+int dl_eager_step(const dl_desc* desc, void* S, const dl_token* tok, float* o,
                   const int32_t* slots, int32_t n, hipStream_t stream);
 
 /* One DeltaLog decode step (Alg. 1) for the listed slots: per (slot, head) read the

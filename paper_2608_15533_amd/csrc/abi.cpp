@@ -26,6 +26,7 @@ int check_desc(const dl_desc* d) {
   // One workgroup per (token row, head): the grid must fit a 32-bit dimension.
   if (int64_t(d->num_slots) * d->heads > int64_t(0x7fffffff)) return DL_E_SHAPE;
   if (d->in_dtype != DL_F32 && d->in_dtype != DL_BF16) return DL_E_DTYPE;
+  if (d->state_dtype != DL_F32 && d->state_dtype != DL_BF16) return DL_E_DTYPE;
   if (d->op == DL_OP_RWKV6) {
     if (d->u_log_dtype != d->in_dtype) return DL_E_DTYPE;   // U_log holds copies of v
   } else {
@@ -99,11 +100,12 @@ void set_token(KParams& p, const dl_token* t) {
 int launch(const dl_desc* d, int mode, const KParams& p, hipStream_t stream) {
   if (p.n == 0) return DL_OK;
   const bool bf16 = d->in_dtype == DL_BF16;
+  const bool sbf16 = d->state_dtype == DL_BF16;
   hipError_t e = hipErrorInvalidValue;
   switch (d->op) {
-    case DL_OP_GDN: e = dl::launch_gdn(mode, d->dk, d->dv, bf16, p, stream); break;
-    case DL_OP_KDA: e = dl::launch_kda(mode, d->dk, d->dv, bf16, p, stream); break;
-    case DL_OP_RWKV6: e = dl::launch_rwkv6(mode, d->dk, d->dv, bf16, p, stream); break;
+    case DL_OP_GDN: e = dl::launch_gdn(mode, d->dk, d->dv, bf16, sbf16, p, stream); break;
+    case DL_OP_KDA: e = dl::launch_kda(mode, d->dk, d->dv, bf16, sbf16, p, stream); break;
+    case DL_OP_RWKV6: e = dl::launch_rwkv6(mode, d->dk, d->dv, bf16, sbf16, p, stream); break;
   }
   return e == hipSuccess ? DL_OK : DL_E_HIP;
 }
@@ -134,7 +136,7 @@ const char* dl_status_str(int status) {
   return "unknown dl_status";
 }
 
-int dl_eager_step(const dl_desc* desc, float* S, const dl_token* tok, float* o,
+int dl_eager_step(const dl_desc* desc, void* S, const dl_token* tok, float* o,
                   const int32_t* slots, int32_t n, hipStream_t stream) {
   DL_TRY(check_desc(desc));
   DL_TRY(check_rows(desc, slots, n));

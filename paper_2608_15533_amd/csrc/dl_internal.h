@@ -14,7 +14,7 @@ enum ModeId { M_EAGER = 0, M_STEP = 1, M_MERGE = 2, M_FLUSH = 3, M_READOUT = 4 }
 
 // Everything a kernel needs, passed by value (all pointers are device pointers).
 struct KParams {
-  float* S;              // [B,H,dk,dv] dense base (or the eager dense state)
+  void* S;               // [B,H,dk,dv] dense base (or the eager dense state), fp32 or bf16
   float* ell;            // [B,H,dl]
   void* k_log;           // [B,H,C,dk]
   void* u_log;           // [B,H,C,dv]
@@ -32,10 +32,13 @@ struct KParams {
   int32_t n, B, H, C;
 };
 
-// Launch the kernel for (op, mode, dk, dv, input dtype) with one workgroup per
-// (token row, head).  Returns the hipError_t of the launch.
-hipError_t launch_gdn(int mode, int dk, int dv, bool bf16, const KParams& p, hipStream_t s);
-hipError_t launch_kda(int mode, int dk, int dv, bool bf16, const KParams& p, hipStream_t s);
-hipError_t launch_rwkv6(int mode, int dk, int dv, bool bf16, const KParams& p, hipStream_t s);
+// Launch the kernel for (op, mode, dk, dv, input dtype, state dtype) with one
+// workgroup per (token row, head).  Returns the hipError_t of the launch.
+hipError_t launch_gdn(int mode, int dk, int dv, bool bf16, bool state_bf16, const KParams& p,
+                      hipStream_t s);
+hipError_t launch_kda(int mode, int dk, int dv, bool bf16, bool state_bf16, const KParams& p,
+                      hipStream_t s);
+hipError_t launch_rwkv6(int mode, int dk, int dv, bool bf16, bool state_bf16, const KParams& p,
+                        hipStream_t s);
 
 }  // namespace dl

@@ -122,23 +122,53 @@ __device__ __forceinline__ float dl_exp(float x) { return __expf(x); }
 constexpr int kStateCachePolicy = DL_NT_STATE ? 2 : 0;   // 2 = non-temporal
 constexpr int kRawBufferFlags = 0x00020000;                // 32-bit data format, raw access
 
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t state_rsrc(float* base, uint32_t bytes) {
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t state_rsrc(void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(base, 0, int(bytes), kRawBufferFlags);
 }
 
-__device__ __forceinline__ float4 ld_state(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
-  const auto w = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, kStateCachePolicy);
-  return make_float4(__uint_as_float(w[0]), __uint_as_float(w[1]), __uint_as_float(w[2]),
-                     __uint_as_float(w[3]));
+// Round fp32 to bf16, nearest even (finite values).
+__device__ __forceinline__ uint32_t bf16_rne(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
 }
 
-__device__ __forceinline__ void st_state(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff,
-                                         float4 v) {
-  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-  const u32x4 w = {__float_as_uint(v.x), __float_as_uint(v.y), __float_as_uint(v.z),
-                   __float_as_uint(v.w)};
-  __builtin_amdgcn_raw_buffer_store_b128(w, r, voff, soff, kStateCachePolicy);
-}
+// Four consecutive state elements of one row, as held by one lane between the load and
+// the store.  fp32 state: one 16-byte access; bf16 state: one 8-byte access, widened to
+// fp32 on use and rounded (nearest even) on store.
+template <typename TS> struct StateQuad;
+template <> struct StateQuad<float> {
+  float4 w;
+  __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+    const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, kStateCachePolicy);
+    w = make_float4(__uint_as_float(v[0]), __uint_as_float(v[1]), __uint_as_float(v[2]),
+                    __uint_as_float(v[3]));
+  }
+  __device__ __forceinline__ float4 get() const { return w; }
+  static __device__ __forceinline__ void store(__amdgpu_buffer_rsrc_t r, uint32_t voff,
+                                               uint32_t soff, float4 v) {
+    typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+    const u32x4 x = {__float_as_uint(v.x), __float_as_uint(v.y), __float_as_uint(v.z),
+                     __float_as_uint(v.w)};
+    __builtin_amdgcn_raw_buffer_store_b128(x, r, voff, soff, kStateCachePolicy);
+  }
+};
+template <> struct StateQuad<uint16_t> {
+  uint2 w;
+  __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+    const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, kStateCachePolicy);
+    w = make_uint2(v[0], v[1]);
+  }
+  __device__ __forceinline__ float4 get() const {
+    return make_float4(__uint_as_float(w.x << 16), __uint_as_float(w.x & 0xffff0000u),
+                       __uint_as_float(w.y << 16), __uint_as_float(w.y & 0xffff0000u));
+  }
+  static __device__ __forceinline__ void store(__amdgpu_buffer_rsrc_t r, uint32_t voff,
+                                               uint32_t soff, float4 v) {
+    typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+    const u32x2 x = {bf16_rne(v.x) | (bf16_rne(v.y) << 16), bf16_rne(v.z) | (bf16_rne(v.w) << 16)};
+    __builtin_amdgcn_raw_buffer_store_b64(x, r, voff, soff, kStateCachePolicy);
+  }
+};
 
 // N consecutive elements (N a multiple of 8) widened to fp32, loaded with 16-byte accesses.
 template <int N>
@@ -274,7 +304,7 @@ struct UType<OP_RWKV6, TIN> { using type = TIN; };  // RWKV6: U_log holds exact 
 // Every global load a workgroup needs is issued before its first barrier: the token
 // rows, the state tile, the first pass of log keys/snapshots and the first log values
 // of the replay; only the live length (and the slot id, for slot lists) precede them.
-template <int OP, int DK, int DV, int MODE, typename TIN>
+template <int OP, int DK, int DV, int MODE, typename TIN, typename TS>
 __global__ __launch_bounds__(threads_per_head(DK, DV)) DL_OCCUPANCY
 void deltalog_kernel(KParams p) {
   using CF = Cfg<OP, DK, DV, MODE>;
@@ -360,13 +390,14 @@ void deltalog_kernel(KParams p) {
   // tile never waits for the length.  DL_LOG_FIRST = 1 waits for the length first and
   // issues the log entries ahead of the tile, so the coefficient pass does not wait
   // for the tile.
-  const auto srs = state_rsrc(p.S + sh * size_t(DK) * DV, DK * DV * 4);
-  const uint32_t toff = uint32_t(rg * DV + 4 * cg) * 4;   // this lane's byte offset in a row block
-  constexpr uint32_t kRowBlock = NRG * DV * 4;             // bytes between row j and row j+1 of a lane
-  float4 t[RPT];
+  TS* const Sh = static_cast<TS*>(p.S) + sh * size_t(DK) * DV;
+  const auto srs = state_rsrc(Sh, DK * DV * sizeof(TS));
+  const uint32_t toff = uint32_t(rg * DV + 4 * cg) * sizeof(TS);   // lane's byte offset in a row block
+  constexpr uint32_t kRowBlock = NRG * DV * sizeof(TS);             // bytes from row j to row j+1 of a lane
+  StateQuad<TS> t[RPT];
   if constexpr (!DL_LOG_FIRST) {
 #pragma unroll
-    for (int j = 0; j < RPT; ++j) t[j] = ld_state(srs, toff, j * kRowBlock);
+    for (int j = 0; j < RPT; ++j) t[j].load(srs, toff, j * kRowBlock);
     asm volatile("" ::: "memory");
     sched_fence();
   }
@@ -395,9 +426,9 @@ void deltalog_kernel(KParams p) {
   // re-read entry L-1 (same cache lines), an empty log reads entry 0, and a log of
   // capacity 0 reads the head's own state tile instead; such values are never used.
   const int Lm1 = L > 0 ? L - 1 : 0;
-  const TIN* Kp = C > 0 ? Kb : reinterpret_cast<const TIN*>(p.S + sh * size_t(DK) * DV);
-  const float* Lp = C > 0 ? Lb : p.S + sh * size_t(DK) * DV;
-  const TU* Up = C > 0 ? Ub : reinterpret_cast<const TU*>(p.S + sh * size_t(DK) * DV);
+  const TIN* Kp = C > 0 ? Kb : reinterpret_cast<const TIN*>(Sh);
+  const float* Lp = C > 0 ? Lb : reinterpret_cast<const float*>(Sh);
+  const TU* Up = C > 0 ? Ub : reinterpret_cast<const TU*>(Sh);
   if constexpr (CF::REPLAYS && DL_PREFETCH_KEYS && (DL == 1 || kPrefetchPerKey)) {
     const int ek = min(e_, Lm1);
     kr_raw.load(Kp + size_t(ek) * DK + c_ * RPL);
@@ -412,7 +443,7 @@ void deltalog_kernel(KParams p) {
   if constexpr (DL_LOG_FIRST) {
     sched_fence();
 #pragma unroll
-    for (int j = 0; j < RPT; ++j) t[j] = ld_state(srs, toff, j * kRowBlock);
+    for (int j = 0; j < RPT; ++j) t[j].load(srs, toff, j * kRowBlock);
   }
   sched_fence();
   const float kf = to_f32(k_raw), qf = to_f32(q_raw);
@@ -528,8 +559,9 @@ void deltalog_kernel(KParams p) {
 #pragma unroll
     for (int j = 0; j < RPT; ++j) {
       const int r = rg + NRG * j;
-      if constexpr (CF::NEEDS_C) cv = fma4(s_xk[r], t[j], cv);
-      ov = fma4(s_xq[r], t[j], ov);
+      const float4 sj = t[j].get();
+      if constexpr (CF::NEEDS_C) cv = fma4(s_xk[r], sj, cv);
+      ov = fma4(s_xq[r], sj, ov);
     }
     if constexpr (CF::HAS_LOG) {
       // Each log value row is read by exactly one row group; a merging workgroup keeps
@@ -624,11 +656,12 @@ void deltalog_kernel(KParams p) {
 
   // ---- 8b. materialise (Eq. 6 / Eq. 7 / Eq. 3) ---------------------------------------
   if constexpr (CF::CAN_MERGE) {
+    float4 m[RPT];                                  // the materialised rows, fp32
 #pragma unroll
     for (int j = 0; j < RPT; ++j) {
       const int r = rg + NRG * j;
-      t[j] = s_em[r] * t[j];
-      if constexpr (CF::HAS_TOKEN) t[j] = fma4(s_kf[r], bv, t[j]);
+      m[j] = s_em[r] * t[j].get();
+      if constexpr (CF::HAS_TOKEN) m[j] = fma4(s_kf[r], bv, m[j]);
     }
     if constexpr (CF::MERGES_LOG) {
       for (int i0 = 0; i0 < L; i0 += CF::CH) {     // uniform trip count
@@ -661,16 +694,16 @@ void deltalog_kernel(KParams p) {
           for (int j = 0; j < RPT; ++j) {
             const int r = rg + NRG * j;
             const float4 kt = *reinterpret_cast<const float4*>(&s_kt[r * CF::KTS + ii]);
-            t[j] = fma4(kt.x, u0, t[j]);
-            t[j] = fma4(kt.y, u1, t[j]);
-            t[j] = fma4(kt.z, u2, t[j]);
-            t[j] = fma4(kt.w, u3, t[j]);
+            m[j] = fma4(kt.x, u0, m[j]);
+            m[j] = fma4(kt.y, u1, m[j]);
+            m[j] = fma4(kt.z, u2, m[j]);
+            m[j] = fma4(kt.w, u3, m[j]);
           }
         }
       }
     }
 #pragma unroll
-    for (int j = 0; j < RPT; ++j) st_state(srs, toff, j * kRowBlock, t[j]);
+    for (int j = 0; j < RPT; ++j) StateQuad<TS>::store(srs, toff, j * kRowBlock, m[j]);
     if constexpr (CF::HAS_LOG) {
       for (int x = tid; x < DL; x += NT) p.ell[sh * DL + x] = 0.f;
       if (tid == 0) p.len[sh] = 0;

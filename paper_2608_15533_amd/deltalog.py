@@ -27,7 +27,7 @@ if not os.path.exists(LIB_PATH):
 _lib = ctypes.CDLL(LIB_PATH)
 
 # ----------------------------------------------------------------- constants (deltalog.h)
-DL_ABI_VERSION = 1
+DL_ABI_VERSION = 2
 DL_MAX_MERGE_INTERVAL = 64
 DL_OK, DL_E_NULL, DL_E_SHAPE, DL_E_DTYPE, DL_E_ALIGN, DL_E_UNSUPPORTED, DL_E_HIP, DL_E_VERSION = (
     0, -1, -2, -3, -4, -5, -6, -7)
@@ -46,7 +46,7 @@ class dl_desc(ctypes.Structure):
                 ("num_slots", ctypes.c_int32), ("heads", ctypes.c_int32),
                 ("dk", ctypes.c_int32), ("dv", ctypes.c_int32),
                 ("merge_interval", ctypes.c_int32), ("in_dtype", ctypes.c_int32),
-                ("u_log_dtype", ctypes.c_int32)]
+                ("u_log_dtype", ctypes.c_int32), ("state_dtype", ctypes.c_int32)]
 
 
 class dl_state(ctypes.Structure):
@@ -96,11 +96,15 @@ if dl_abi_version() != DL_ABI_VERSION:
 
 
 # ----------------------------------------------------------------- descriptors
-def make_desc(op, B, H, dk, dv, M, in_dtype="bf16"):
+def make_desc(op, B, H, dk, dv, M, in_dtype="bf16", state_dtype="f32"):
     """dl_desc for operator ``op`` ("gdn"/"kda"/"rwkv6") with merge interval M."""
     u_dtype = in_dtype if op == "rwkv6" else "f32"
     return dl_desc(DL_ABI_VERSION, OP_IDS[op], B, H, dk, dv, M, DTYPE_IDS[in_dtype],
-                   DTYPE_IDS[u_dtype])
+                   DTYPE_IDS[u_dtype], DTYPE_IDS[state_dtype])
+
+
+def state_torch_dtype(desc):
+    return torch.bfloat16 if desc.state_dtype == DL_BF16 else torch.float32
 
 
 def _ptr(t):
@@ -123,9 +127,10 @@ def _need(t, name, dtype, shape, device=None):
 class DeltaLogState:
     """Device buffers of the physical state (Sec. 3.1), allocated with torch.
 
-    S [B,H,dk,dv] f32, ell [B,H,dl] f32, k_log [B,H,C,dk] in_dtype, u_log [B,H,C,dv],
-    lam_log [B,H,C,dl] f32, len [B,H] int32, err [1] int32.  ``S`` starts as a copy of
-    ``S0`` (the prefill state); the log starts empty (Sec. 4 slot lifecycle).
+    S [B,H,dk,dv] state dtype, ell [B,H,dl] f32, k_log [B,H,C,dk] in_dtype,
+    u_log [B,H,C,dv], lam_log [B,H,C,dl] f32, len [B,H] int32, err [1] int32.  ``S``
+    starts as a copy of ``S0`` (the prefill state, converted to the state dtype); the
+    log starts empty (Sec. 4 slot lifecycle).
     """
 
     def __init__(self, desc, S0=None, device="cuda"):
@@ -136,7 +141,9 @@ class DeltaLogState:
         in_t = torch.bfloat16 if desc.in_dtype == DL_BF16 else torch.float32
         u_t = torch.bfloat16 if desc.u_log_dtype == DL_BF16 else torch.float32
         f32 = dict(dtype=torch.float32, device=device)
-        self.S = torch.zeros((B, H, dk, dv), **f32) if S0 is None else S0.to(device=device, dtype=torch.float32).contiguous().clone()
+        st = state_torch_dtype(desc)
+        self.S = (torch.zeros((B, H, dk, dv), dtype=st, device=device) if S0 is None else
+                  S0.to(device=device, dtype=st).contiguous().clone())
         self.ell = torch.zeros((B, H, dl), **f32)
         self.k_log = torch.zeros((B, H, max(C, 0), dk), dtype=in_t, device=device)
         self.u_log = torch.zeros((B, H, max(C, 0), dv), dtype=u_t, device=device)
@@ -197,7 +204,7 @@ def dl_eager_step(desc, S, tok, o, slots=None, stream=None):
     """Eager dense step (Eq. 3) on S [B,H,dk,dv]; writes o [n,H,dv] f32."""
     sp, n = _rows(desc, slots, tok.n)
     _need(o, "o", torch.float32, (n, desc.heads, desc.dv))
-    _need(S, "S", torch.float32, (desc.num_slots, desc.heads, desc.dk, desc.dv))
+    _need(S, "S", state_torch_dtype(desc), (desc.num_slots, desc.heads, desc.dk, desc.dv))
     _check(_lib.dl_eager_step(ctypes.byref(desc), _ptr(S), ctypes.byref(tok.struct), _ptr(o),
                               sp, n, _stream(stream)), "dl_eager_step")
 

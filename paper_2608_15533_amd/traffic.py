@@ -8,7 +8,8 @@ phase, with the precisions the library uses:
   activation dtype, beta (fp32, delta rule only) and the step log-decay lambda (fp32,
   one value per head or one per key).  The RWKV6 bonus u is a per-head parameter shared
   by every slot and is not counted (as in the paper's model).
-* dense state ``C_state``: 4 * dk * dv bytes (fp32) per head.
+* dense state ``C_state``: p_S * dk * dv bytes per head (p_S = 4 for fp32 state, 2 for
+  bf16 state).
 * one log entry ``C_entry``: p_K dk + p_U dv + 4 d_lambda bytes (Eq. 9), with K_log in the
   activation dtype and U_log fp32 for GDN/KDA, activation dtype for RWKV6.
 * cumulative log-decay ``C_decay``: 4 d_lambda bytes, read and written every DeltaLog step.
@@ -39,11 +40,11 @@ class HeadTraffic:
         return self.read + self.write
 
 
-def _sizes(op, dk, dv, in_dtype):
+def _sizes(op, dk, dv, in_dtype, state_dtype="f32"):
     pin = DTYPE_BYTES[in_dtype]
     dl = 1 if op == "gdn" else dk
     common = pin * (2 * dk + dv) + 4 * dl + (4 if op in ("gdn", "kda") else 0)
-    state = 4 * dk * dv
+    state = DTYPE_BYTES[state_dtype] * dk * dv
     p_u = 4 if op in ("gdn", "kda") else pin
     entry = pin * dk + p_u * dv + 4 * dl
     decay = 4 * dl
@@ -51,49 +52,49 @@ def _sizes(op, dk, dv, in_dtype):
     return common, state, entry, decay, out
 
 
-def eager_bytes(op, dk, dv, in_dtype="bf16"):
+def eager_bytes(op, dk, dv, in_dtype="bf16", state_dtype="f32"):
     """Bytes one eager dense step moves for one head (Eq. 8 plus the output)."""
-    common, state, _, _, out = _sizes(op, dk, dv, in_dtype)
+    common, state, _, _, out = _sizes(op, dk, dv, in_dtype, state_dtype)
     return HeadTraffic(read=common + state, write=state + out)
 
 
-def append_bytes(op, dk, dv, L, in_dtype="bf16"):
+def append_bytes(op, dk, dv, L, in_dtype="bf16", state_dtype="f32"):
     """Bytes of a DeltaLog append step taken at live length L."""
-    common, state, entry, decay, out = _sizes(op, dk, dv, in_dtype)
+    common, state, entry, decay, out = _sizes(op, dk, dv, in_dtype, state_dtype)
     return HeadTraffic(read=common + state + decay + L * entry, write=entry + decay + out)
 
 
-def merge_bytes(op, dk, dv, L, in_dtype="bf16"):
+def merge_bytes(op, dk, dv, L, in_dtype="bf16", state_dtype="f32"):
     """Bytes of a DeltaLog merge step that folds L live entries (plus the token)."""
-    common, state, entry, decay, out = _sizes(op, dk, dv, in_dtype)
+    common, state, entry, decay, out = _sizes(op, dk, dv, in_dtype, state_dtype)
     return HeadTraffic(read=common + state + decay + L * entry, write=state + decay + out)
 
 
-def step_bytes(op, dk, dv, M, L, in_dtype="bf16"):
+def step_bytes(op, dk, dv, M, L, in_dtype="bf16", state_dtype="f32"):
     """Bytes of the Alg. 1 step at live length L: append if L < M-1, else merge."""
     if L < M - 1:
-        return append_bytes(op, dk, dv, L, in_dtype)
-    return merge_bytes(op, dk, dv, L, in_dtype)
+        return append_bytes(op, dk, dv, L, in_dtype, state_dtype)
+    return merge_bytes(op, dk, dv, L, in_dtype, state_dtype)
 
 
-def cycle_bytes(op, dk, dv, M, in_dtype="bf16"):
+def cycle_bytes(op, dk, dv, M, in_dtype="bf16", state_dtype="f32"):
     """Total bytes of one full cycle (M-1 appends at L = 0..M-2, one merge at L = M-1)."""
     r = w = 0
     for L in range(M):
-        t = step_bytes(op, dk, dv, M, L, in_dtype)
+        t = step_bytes(op, dk, dv, M, L, in_dtype, state_dtype)
         r += t.read
         w += t.write
     return HeadTraffic(read=r, write=w)
 
 
-def amortized_bytes_per_token(op, dk, dv, M, in_dtype="bf16"):
+def amortized_bytes_per_token(op, dk, dv, M, in_dtype="bf16", state_dtype="f32"):
     """Average bytes per head-token over a cycle (the Eq. 10 quantity, plus outputs)."""
-    c = cycle_bytes(op, dk, dv, M, in_dtype)
+    c = cycle_bytes(op, dk, dv, M, in_dtype, state_dtype)
     return c.total / M
 
 
-def state_write_ratio(op, dk, dv, M, in_dtype="bf16"):
+def state_write_ratio(op, dk, dv, M, in_dtype="bf16", state_dtype="f32"):
     """Eager / DeltaLog state-write bytes per token, outputs excluded: M / (1 + eps)."""
-    _, state, entry, decay, _ = _sizes(op, dk, dv, in_dtype)
+    _, state, entry, decay, _ = _sizes(op, dk, dv, in_dtype, state_dtype)
     dl_writes = (state + (M - 1) * entry + M * decay) / M
     return state / dl_writes

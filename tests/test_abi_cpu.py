@@ -36,7 +36,7 @@ def test_header_functions_are_exported():
 
 
 def test_version_and_status_strings():
-    assert D.dl_abi_version() == D.DL_ABI_VERSION == 1
+    assert D.dl_abi_version() == D.DL_ABI_VERSION == 2
     for code in range(0, -8, -1):
         s = D.dl_status_str(code)
         assert s.startswith("DL_") and s != "unknown dl_status"
@@ -75,7 +75,7 @@ def test_null_descriptor():
 
 
 @pytest.mark.parametrize("field,value,code", [
-    ("abi_version", 2, D.DL_E_VERSION),
+    ("abi_version", 1, D.DL_E_VERSION),
     ("op", 3, D.DL_E_UNSUPPORTED),
     ("dk", 96, D.DL_E_UNSUPPORTED),
     ("dv", 256, D.DL_E_UNSUPPORTED),
@@ -85,9 +85,26 @@ def test_null_descriptor():
     ("heads", 0, D.DL_E_SHAPE),
     ("in_dtype", 7, D.DL_E_DTYPE),
     ("u_log_dtype", D.DL_BF16, D.DL_E_DTYPE),        # GDN U_log must be fp32
+    ("state_dtype", 5, D.DL_E_DTYPE),
 ])
 def test_descriptor_rejections(field, value, code):
     assert append(desc(**{field: value})) == code
+
+
+def test_descriptor_layout_matches_header():
+    """The ctypes mirror of dl_desc has the header's field order and size (10 int32)."""
+    text = open(HEADER).read()
+    body = re.search(r"typedef struct \{(.*?)\} dl_desc;", text, flags=re.S).group(1)
+    body = re.sub(r"/\*.*?\*/", "", body, flags=re.S)
+    names = re.findall(r"int32_t\s+([a-z_]+(?:\s*,\s*[a-z_]+)*)\s*;", body)
+    fields = [n.strip() for group in names for n in group.split(",")]
+    assert fields == [f for f, _ in D.dl_desc._fields_]
+    assert ctypes.sizeof(D.dl_desc) == 4 * len(fields) == 40
+
+
+def test_bf16_state_descriptor_is_accepted():
+    """state_dtype = BF16 passes validation (the call then stops at a misaligned output)."""
+    assert append(desc(state_dtype=D.DL_BF16), o=A + 4) == D.DL_E_ALIGN
 
 
 def test_rwkv6_u_log_dtype_must_match_input():

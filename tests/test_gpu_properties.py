@@ -61,7 +61,7 @@ def run_deltalog(desc, S0, xs, u, slots_per_step=None):
 
 def run_eager(desc, S0, xs, u):
     dl = D()
-    S = to_dev(S0, torch.float32)
+    S = to_dev(S0, dl.state_torch_dtype(desc))
     outs = []
     for x in xs:
         tok = token(desc, x, u)
@@ -336,3 +336,24 @@ def test_zero_rows_is_a_no_op_on_device():
     after = _state_arrays(st)
     for k in before:
         np.testing.assert_array_equal(before[k], after[k], err_msg=k)
+
+
+@pytest.mark.parametrize("op", OPS)
+def test_exact_dyadic_bf16_state_bitwise(op):
+    """bf16 state: with beta = 1 every stored value is a small integer, exact in bf16, so
+    the GPU must still equal the oracle bit for bit (outputs, merged base, eager state)."""
+    B, H, M, steps, dk = 3, 2, 4, 8, 128
+    S0, xs, u = dyadic_inputs(op, B, H, dk, dk, steps, seed=17 + OPS.index(op))
+    for x in xs:
+        if x["beta"] is not None:
+            x["beta"][:] = 1.0
+    desc = D().make_desc(op, B, H, dk, dk, M, "bf16", "bf16")
+    outs, st = run_deltalog(desc, S0, xs, u)
+    ref_o, ref_S = oracle_run(op, S0, xs, u)
+    for t in range(steps):
+        np.testing.assert_array_equal(outs[t].astype(np.float64), ref_o[t], err_msg=f"step {t}")
+    np.testing.assert_array_equal(st.S.float().cpu().numpy().astype(np.float64), ref_S[-1])
+    eo, eS = run_eager(desc, S0, xs, u)
+    for t in range(steps):
+        np.testing.assert_array_equal(eo[t].astype(np.float64), ref_o[t], err_msg=f"eager {t}")
+    np.testing.assert_array_equal(eS.float().cpu().numpy().astype(np.float64), ref_S[-1])
