@@ -64,6 +64,10 @@ def parse():
     ap.add_argument("--steps", type=int, default=256)
     ap.add_argument("--warmup", type=int, default=32)
     ap.add_argument("--replicas", type=int, default=0, help="layer states (0: workload default)")
+    ap.add_argument("--merge-interval", type=int, default=0,
+                    help="override the workload's merge interval M (0: workload default)")
+    ap.add_argument("--batch", type=int, default=0,
+                    help="override the workload's sequence count B (0: workload default)")
     ap.add_argument("--state-dtype", default="f32", choices=("f32", "bf16"),
                     help="dtype of the dense state (bf16: rounded on every store)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -172,6 +176,12 @@ def main():
     from paper_2608_15533_amd import workloads as W
 
     w, R = workloads()[args.workload]
+    if args.merge_interval or args.batch:
+        w = w.with_(M=args.merge_interval or w.M, B=args.batch or w.B)
+        # enough layer states for a working set of at least 1 GiB (4x the last-level cache)
+        per_layer = w.B * w.H * (w.dk * w.dv * (2 if args.state_dtype == "bf16" else 4)
+                                 + (w.M - 1) * (w.dk + w.dv) * 4)
+        R = max(2, -(-(1 << 30) // per_layer)) if w.layers == 1 else R
     R = args.replicas or R
     K, WU = args.steps, args.warmup
     dev = "cuda"
@@ -331,7 +341,9 @@ def main():
                          f"{w.in_dtype} q/k/v, merge interval "
                          f"M={w.M}" + (f", {w.layers} layers, staggered log fill"
                                        if w.layers > 1 else "")),
-            "name": args.workload, "op": w.op, "batch": w.B, "heads": w.H, "dk": w.dk,
+            "name": args.workload + (f" M={w.M}" if args.merge_interval else "")
+                    + (f" B={w.B}" if args.batch else ""),
+            "op": w.op, "batch": w.B, "heads": w.H, "dk": w.dk,
             "dv": w.dv, "merge_interval": w.M, "in_dtype": w.in_dtype, "state_dtype": sd,
             "layer_states": R, "state_MiB_per_layer": state_mib,
             "working_set_MiB": round(sum(t.numel() * t.element_size() for st in states

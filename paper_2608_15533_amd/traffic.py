@@ -98,3 +98,10 @@ def state_write_ratio(op, dk, dv, M, in_dtype="bf16", state_dtype="f32"):
     _, state, entry, decay, _ = _sizes(op, dk, dv, in_dtype, state_dtype)
     dl_writes = (state + (M - 1) * entry + M * decay) / M
     return state / dl_writes
+
+
+def byte_optimal_merge_interval(op, dk, dv, in_dtype="bf16", state_dtype="f32", max_M=64):
+    """The merge interval that minimises the amortised bytes per token (Eq. 10's
+    trade-off: the dense write amortised over M against the growing replay)."""
+    return min(range(1, max_M + 1),
+               key=lambda M: amortized_bytes_per_token(op, dk, dv, M, in_dtype, state_dtype))

@@ -63,3 +63,17 @@ def test_benefit_condition():
     for M in range(2, 33):
         assert T.amortized_bytes_per_token("gdn", 128, 128, M) < T.eager_bytes("gdn", 128, 128).total
     assert T.amortized_bytes_per_token("gdn", 128, 128, 1) > T.eager_bytes("gdn", 128, 128).total
+
+
+def test_byte_optimal_merge_interval():
+    """Eq. 10's optimum for the tested shapes (bf16 activations, fp32 state): an interior
+    minimum that is larger for head-wise scalar decay (compact metadata) than for
+    per-key decay, and no larger than where the benefit condition still holds."""
+    gdn = T.byte_optimal_merge_interval("gdn", 128, 128)
+    kda = T.byte_optimal_merge_interval("kda", 128, 128)
+    rwkv6 = T.byte_optimal_merge_interval("rwkv6", 64, 64)
+    assert (gdn, kda, rwkv6) == (13, 10, 8)
+    for op, d, m in (("gdn", 128, gdn), ("kda", 128, kda), ("rwkv6", 64, rwkv6)):
+        a = [T.amortized_bytes_per_token(op, d, d, M) for M in range(1, 65)]
+        assert a[m - 1] == min(a)
+        assert a[m - 1] < T.eager_bytes(op, d, d).total
