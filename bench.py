@@ -72,6 +72,15 @@ def parse():
                     help="dtype of the dense state (bf16: rounded on every store)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--decode-loop", default="", metavar="MODES",
+                    help="instead of the kernel bench: time the decode loop (slot allocator, "
+                         "graph-captured steps) under comma-separated scheduling modes "
+                         "(fused, phased, phased_concurrent; 'all'), with and without graphs")
+    ap.add_argument("--layers", type=int, default=24, help="decode-loop layers")
+    ap.add_argument("--merge-first", action="store_true",
+                    help="decode loop, fused mode: rows of merging slots first (default: slot order)")
+    ap.add_argument("--uniform", action="store_true",
+                    help="decode loop: admit every sequence at once (default: staggered)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (5 times); used to "
                          "scale the HBM byte counters of a profiler run")
@@ -158,6 +167,108 @@ def cpu_baseline(w, budget_s):
     }
 
 
+def decode_loop(args):
+    """Decode-loop throughput: a GDN stack of ``--layers`` layers, B slots x 32 heads of
+    128^2, M = 16 (or the overrides), bf16 q/k/v, fp32 state.  Sequences are admitted
+    B/M per step over the first M steps (staggered logs, so every step mixes appends and
+    merges) or all at once (``--uniform``).  Each timed step is one plan + one decode
+    token through every layer; token inputs stay in the engine's fixed buffers (their
+    values do not change any kernel's cost).  Prints one JSON line with every mode."""
+    import torch
+    from paper_2608_15533_amd import decode
+    from paper_2608_15533_amd import deltalog as D
+    from paper_2608_15533_amd import traffic as T
+
+    B = args.batch or 256
+    M = args.merge_interval or 16
+    layers = args.layers
+    H, dk, dv = 32, 128, 128
+    K, WU = args.steps, args.warmup
+    modes = decode.MODES if args.decode_loop == "all" else tuple(args.decode_loop.split(","))
+    desc = D.make_desc("gdn", B, H, dk, dv, M, "bf16")
+    torch.cuda.set_device(0)
+    res = {}
+    for mode in modes:
+        for graphs in (True, False):
+            eng = decode.DecodeEngine(desc, layers, mode=mode, graphs=graphs,
+                                      merge_first=args.merge_first)
+            gen = torch.Generator(device="cuda")
+            gen.manual_seed(20261202)
+            for layer in range(layers):
+                x = eng.inputs[layer]
+                qk = torch.randn((2, B, H, dk), generator=gen, device="cuda")
+                qk = qk / qk.norm(dim=-1, keepdim=True)
+                x.q.copy_(qk[0])
+                x.k.copy_(qk[1])
+                x.v.copy_(torch.randn((B, H, dv), generator=gen, device="cuda"))
+                g = torch.randn((B, H), generator=gen, device="cuda")
+                x.lam.copy_(torch.nn.functional.logsigmoid(3.0 + 0.5 * g))
+                x.beta.copy_(torch.sigmoid(torch.randn((B, H), generator=gen, device="cuda")))
+                st = eng.states[layer]
+                st.S.copy_(torch.randn(st.S.shape, generator=gen, device="cuda") * 0.02)
+            per_step = B if args.uniform else max(1, -(-B // M))
+            steps_run = 0
+            while eng.sched.free_slots:
+                for _ in range(min(per_step, eng.sched.free_slots)):
+                    slot = eng.sched.admit()           # the base already holds a state
+                    for st in eng.states:
+                        st.ell[slot].zero_()
+                        st.len[slot].zero_()
+                eng.schedule()
+                eng.step()
+                steps_run += 1
+            for _ in range(WU):
+                eng.schedule()
+                eng.step()
+            torch.cuda.synchronize()
+            # algorithmic bytes of the timed steps, from a copy of the live-length mirror
+            live = list(eng.sched.live)
+            C = M - 1
+            nbytes = 0
+            for _ in range(K):
+                for s in eng.sched.active:
+                    nbytes += T.step_bytes("gdn", dk, dv, M, live[s]).total
+                    live[s] = 0 if live[s] >= C else live[s] + 1
+            nbytes *= H * layers
+            stream = torch.cuda.current_stream()
+            t0 = torch.cuda.Event(enable_timing=True)
+            t1 = torch.cuda.Event(enable_timing=True)
+            h0 = time.perf_counter()
+            t0.record(stream)
+            for _ in range(K):
+                eng.schedule()
+                eng.step()
+            t1.record(stream)
+            h1 = time.perf_counter()
+            torch.cuda.synchronize()
+            ms = t0.elapsed_time(t1)
+            n = len(eng.sched.active)
+            assert eng.error_words() == [0] * layers
+            res[mode + ("" if graphs else "_direct")] = {
+                "seq_tokens_per_s": round(n * K / (ms * 1e-3), 1),
+                "layer_token_updates_per_s": round(n * layers * K / (ms * 1e-3), 1),
+                "ms_per_step": round(ms / K, 5),
+                "host_ms_per_step": round((h1 - h0) * 1e3 / K, 5),
+                "GB/s": round(nbytes / (ms * 1e-3) / 1e9, 1),
+                "frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                "graphs": len(eng.graph_keys),
+                "replays": eng.replays,
+            }
+            del eng
+            torch.cuda.empty_cache()
+    print(json.dumps({
+        "metric": "decode-loop sequence tokens/s (all layers' state updates per token)",
+        "unit": "tokens/s", "steps": K, "warmup": WU, "data": "synthetic",
+        "config": {"workload": f"GDN {layers}-layer decode loop: B={B} slots, H={H}, "
+                               f"dk=dv={dk}, M={M}, bf16 q/k/v, fp32 state, "
+                               f"{'uniform' if args.uniform else 'staggered'} admission",
+                   "batch": B, "layers": layers, "merge_interval": M,
+                   "fused_row_order": "merging slots first" if args.merge_first else "slot"},
+        "modes": res,
+        "kernel_source_hash": kernel_source_hash(),
+    }), flush=True)
+
+
 def main():
     args = parse()
     if args.copy_calibration:
@@ -167,6 +278,9 @@ def main():
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}): the decode state "
               "update has no cross-GPU step; run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
+    if args.decode_loop:
+        decode_loop(args)
+        return
 
     import ctypes
 

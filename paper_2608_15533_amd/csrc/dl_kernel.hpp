@@ -191,6 +191,12 @@ __device__ __forceinline__ void ld_run(const uint16_t* p, float (&o)[N]) {
 }
 
 constexpr uint32_t kXcds = 8;   // accelerator complex dies of an MI355X
+// (row, head) pairs per XCD chunk: 32 heads' 4-byte metadata is one 128-byte line.
+// 0 gives each XCD a single contiguous range instead.
+#ifndef DL_XCD_CHUNK
+#define DL_XCD_CHUNK 32
+#endif
+constexpr uint32_t kXcdChunk = DL_XCD_CHUNK;
 
 // Raw register images of loads whose conversion to fp32 is deferred: converting right
 // after a load makes the wave wait for it, and (loads completing in issue order) for
@@ -329,13 +335,24 @@ void deltalog_kernel(KParams p) {
   const int tid = threadIdx.x;
   const int H = p.H;
   // Workgroups are dispatched round-robin over the 8 XCDs (each with its own L2).  Map
-  // them so that XCD x owns a contiguous range of (row, head) pairs: the 4-byte
-  // per-head metadata (ell, L, scalar log-decay snapshots) and token scalars of
-  // neighbouring heads then share L2 sectors instead of being written back partially
-  // by eight different caches.
+  // them so that each XCD owns whole chunks of DL_XCD_CHUNK consecutive (row, head)
+  // pairs: the 4-byte per-head metadata (ell, L, scalar log-decay snapshots) and token
+  // scalars of a chunk then fill whole 128-byte lines in one L2 instead of being
+  // written back partially by eight different caches.  Chunks are dealt to the XCDs
+  // in turn, so a run of consecutive slots that merge in the same step (slots admitted
+  // together) is spread over all eight XCDs instead of loading one of them.  Rows past
+  // the last whole round of chunks keep the hardware order.
   uint32_t lin = blockIdx.x;
   const uint32_t nblk = gridDim.x;
-  if (nblk % kXcds == 0) lin = (lin % kXcds) * (nblk / kXcds) + lin / kXcds;
+  if constexpr (kXcdChunk > 0) {
+    const uint32_t full = nblk - nblk % (kXcds * kXcdChunk);
+    if (lin < full) {
+      const uint32_t x = lin % kXcds, j = lin / kXcds;
+      lin = ((j / kXcdChunk) * kXcds + x) * kXcdChunk + j % kXcdChunk;
+    }
+  } else if (nblk % kXcds == 0) {
+    lin = (lin % kXcds) * (nblk / kXcds) + lin / kXcds;   // one contiguous range per XCD
+  }
   const int row = int(lin) / H;                   // token row
   const int h = int(lin) - row * H;               // head
   const int slot = p.slots ? p.slots[row] : row;
