@@ -8,7 +8,8 @@ never imports, links or calls it, and it never imports the product path.
 Contents
 --------
 ``eager``          the dense eager recurrence (Eq. 3 with the Table 1 instantiations for
-                   GDN, KDA and RWKV6) in float64 -- the *definition* the GPU must match.
+                   GDN, KDA, RWKV6, linear attention, RetNet and GLA) in float64 -- the
+                   *definition* the GPU must match.
 ``deltalog_model`` the paper's base-plus-log state machine (Alg. 1, append Eq. 5,
                    merge Eq. 6, invariant Eq. 7) in float64, used to check log contents
                    and the equivalence argument of Sec. 3.2 ("Closure under the recurrence").

@@ -6,7 +6,9 @@ The physical state of Sec. 3.1 for N (slot, head) pairs:
 
     Sbar [N, dk, dv]   dense base, last materialisation
     ell  [N, dl]       cumulative log-decay since that materialisation (dl = 1 for
-                       head-wise scalar decay (GDN), dk for per-key decay (KDA, RWKV6))
+                       head-wise scalar decay (GDN, RetNet) and for linear attention,
+                       whose log-decay is identically zero; dk for per-key decay (KDA,
+                       RWKV6, GLA))
     K    [N, C, dk]    deferred key-side factors a_i       (C = M - 1 live-log capacity)
     U    [N, C, dv]    deferred value-side factors b_i
     Lam  [N, C, dl]    log-decay snapshot taken when entry i was appended
@@ -33,7 +35,7 @@ Eqs. 6 and 7 are written for general L; log slots i >= L are never read.
 
 import numpy as np
 
-from .eager import OPS
+from .eager import DELTA_OPS, OPS, PER_KEY_OPS
 
 
 def _f64(x):
@@ -56,7 +58,7 @@ class DeltaLogModel:
         self.C = self.M - 1
         N, dk, dv = S0.shape
         self.N, self.dk, self.dv = N, dk, dv
-        self.dl = 1 if op == "gdn" else dk
+        self.dl = dk if op in PER_KEY_OPS else 1
         # Freshly initialised slot: dense base from "prefill", empty log (Sec. 4).
         self.Sbar = S0.copy()
         self.ell = np.zeros((N, self.dl))
@@ -133,12 +135,15 @@ class DeltaLogModel:
     def step(self, q, k, v, beta, lam, u=None, force_merge=False, active=None):
         """One decode step of Alg. 1; returns the output o [N, dv].
 
-        ``q`` is the receptance r for RWKV6.  ``lam`` is [N] (GDN) or [N, dk].
+        ``q`` is the receptance r for RWKV6.  ``lam`` is [N] (GDN, RetNet), [N, dk]
+        (KDA, RWKV6, GLA), or None for linear attention (no decay: lambda = 0).
         ``force_merge`` merges every head regardless of L (a merge at L < C).
         ``active`` (bool [N], default all) selects the heads that take this step; the
         others keep their state and get NaN outputs (a partial decode batch).
         """
         active = np.full(self.N, True) if active is None else np.asarray(active, dtype=bool)
+        if self.op == "linattn":
+            lam = np.zeros((self.N, self.dl))
         q, k, v, lam = map(_f64, (q, k, v, lam))
         lam = lam.reshape(self.N, self.dl)
         if np.any(self.L > self.C) or np.any(self.L < 0):
@@ -152,6 +157,12 @@ class DeltaLogModel:
             o = np.einsum("ni,nij->nj", q, S_prev) + bonus[:, None] * v
             ell_new = self.ell + lam                       # Alg. 1: ell <- ell + lambda_t
             a, b = k, v                                    # Table 1: pair (k_t, v_t)
+        elif self.op not in DELTA_OPS:
+            # linear attention, RetNet, GLA: pair (k_t, v_t), post-update output (Eq. 3)
+            ell_new = self.ell + lam                       # Alg. 1: ell <- ell + lambda_t
+            a, b = k, v
+            S_t = self.logical_state(ell_new) + a[:, :, None] * b[:, None, :]
+            o = np.einsum("ni,nij->nj", q, S_t)
         else:
             ell_new = self.ell + lam                       # Alg. 1: ell <- ell + lambda_t
             S_dec = self.logical_state(ell_new)            # = D(lambda_t) S_{t-1}

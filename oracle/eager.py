@@ -9,9 +9,12 @@ The unified one-token decode step (Eq. 3) is
 with the state S in R^{dk x dv}; D scales the *rows* (key dimension) of S.  Table 1
 instantiates (a_t, b_t) and the decay form per operator:
 
-    GDN   : head-wise scalar decay, a = k, b = beta (v - k^T S_old)
-    KDA   : per-key (diagonal) decay, same delta-rule pair as GDN
-    RWKV6 : per-key decay, a = k, b = v (no correction)
+    GDN      : head-wise scalar decay, a = k, b = beta (v - k^T S_old)
+    KDA      : per-key (diagonal) decay, same delta-rule pair as GDN
+    RWKV6    : per-key decay, a = k, b = v (no correction)
+    Linear attention : no decay, a = phi(k), b = v (phi already applied to k)
+    RetNet   : head-wise scalar decay gamma_t = exp(lambda_t), a = k, b = v
+    GLA      : per-key (diagonal) decay, a = k, b = v
 
 Readings taken where the text is silent or ambiguous (each is listed in the design doc):
 
@@ -21,7 +24,8 @@ Readings taken where the text is silent or ambiguous (each is listed in DESIGN.m
   and KDA recurrences apply the correction to the decayed state
   ``D(lambda_t) S_{t-1}``.  This oracle uses the decayed state by default; the literal
   undecayed form is kept behind ``correction="undecayed"`` for diagnostics only.
-* Output timing.  GDN/KDA read out the post-update state ``o = q^T S_t`` (Eq. 3).
+* Output timing.  GDN/KDA, linear attention, RetNet and GLA read out the post-update
+  state ``o = q^T S_t`` (Eq. 3; Eq. 1 for linear attention).
   RWKV6 reads the pre-update state plus the per-head bonus ``u``:
   ``o = r^T (S_{t-1} + diag(u) k v^T)`` -- the standard RWKV6 readout.
 * No query scaling is applied inside the step: any feature map or 1/sqrt(dk) is
@@ -29,13 +33,17 @@ Readings taken where the text is silent or ambiguous (each is listed in DESIGN.m
 
 Shapes (any leading batch dims ``...``, typically ``[N]`` heads):
     S  [..., dk, dv]   q,k,r [..., dk]   v [..., dv]   beta [...]
-    lam [...] (GDN, scalar per head) or [..., dk] (KDA, RWKV6)
+    lam [...] (GDN, RetNet: scalar per head) or [..., dk] (KDA, RWKV6, GLA);
+        ignored for linear attention
     u  [..., dk] (RWKV6 bonus, broadcast from the per-head parameter [H, dk])
 """
 
 import numpy as np
 
-OPS = ("gdn", "kda", "rwkv6")
+OPS = ("gdn", "kda", "rwkv6", "linattn", "retnet", "gla")
+DELTA_OPS = ("gdn", "kda")                  # b = beta (v - correction)
+PER_KEY_OPS = ("kda", "rwkv6", "gla")       # diagonal decay: lambda is [..., dk]
+ADDITIVE_OPS = ("linattn", "retnet", "gla")  # pair (k, v) and post-update readout
 
 
 def _f64(x):
@@ -95,28 +103,51 @@ def rwkv6_step(S, r, k, v, lam, u):
     return S_new, o
 
 
-def eager_step(op, S, q, k, v, beta, lam, u=None, correction="decayed"):
-    """Dispatch one eager step for ``op`` in {"gdn", "kda", "rwkv6"}; returns (S_t, o_t).
-
-    For RWKV6 ``q`` carries the receptance r and ``beta`` is ignored.
+def additive_step(S, q, k, v, lam, decay):
+    """One step of the additive operators of Table 1 (pair (k_t, v_t), no correction)
+    with the post-update readout of Eq. 3:  S_t = T(S_{t-1}) + k v^T,  o = q^T S_t, where
+    T is the identity (``decay`` "none": linear attention, Eq. 1), gamma_t S with
+    gamma_t = exp(lambda_t) (``"scalar"``: RetNet) or D(lambda_t) S (``"diagonal"``: GLA).
     """
-    if op in ("gdn", "kda"):
+    S, q, k, v = map(_f64, (S, q, k, v))
+    dk = S.shape[-2]
+    if decay == "none":
+        Sd = S
+    elif decay in ("scalar", "diagonal"):
+        Sd = row_decay(lam, dk, decay == "diagonal") * S
+    else:
+        raise ValueError(decay)
+    S_new = Sd + k[..., :, None] * v[..., None, :]
+    return S_new, _readout(S_new, q)
+
+
+def eager_step(op, S, q, k, v, beta, lam, u=None, correction="decayed"):
+    """Dispatch one eager step for ``op`` in ``OPS``; returns (S_t, o_t).
+
+    For RWKV6 ``q`` carries the receptance r.  ``beta`` is used by the delta rule only,
+    ``lam`` by every operator but linear attention, ``u`` by RWKV6 only.
+    """
+    if op in DELTA_OPS:
         return gdn_kda_step(S, q, k, v, beta, lam, op == "kda", correction=correction)
     if op == "rwkv6":
         return rwkv6_step(S, q, k, v, lam, u)
+    if op in ADDITIVE_OPS:
+        decay = {"linattn": "none", "retnet": "scalar", "gla": "diagonal"}[op]
+        return additive_step(S, q, k, v, lam, decay)
     raise ValueError(op)
 
 
 def eager_rollout(op, S0, steps, u=None, keep_states=False):
     """Run the eager recurrence over a sequence of step inputs.
 
-    ``steps`` is an iterable of dicts with keys q, k, v, beta, lam (beta unused for
-    RWKV6).  Returns (outputs [T, ..., dv], final state, states or None).
+    ``steps`` is an iterable of dicts with keys q, k, v, beta, lam (beta used by the
+    delta rule only; lam may be None for linear attention).  Returns (outputs
+    [T, ..., dv], final state, states or None).
     """
     S = _f64(S0)
     outs, states = [], []
     for st in steps:
-        S, o = eager_step(op, S, st["q"], st["k"], st["v"], st.get("beta"), st["lam"], u=u)
+        S, o = eager_step(op, S, st["q"], st["k"], st["v"], st.get("beta"), st.get("lam"), u=u)
         outs.append(o)
         if keep_states:
             states.append(S.copy())

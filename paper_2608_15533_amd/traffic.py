@@ -6,13 +6,16 @@ phase, with the precisions the library uses:
 
 * ``T_common``: the current-token inputs both schemes read -- q (or r), k, v in the
   activation dtype, beta (fp32, delta rule only) and the step log-decay lambda (fp32,
-  one value per head or one per key).  The RWKV6 bonus u is a per-head parameter shared
-  by every slot and is not counted (as in the paper's model).
+  one value per head or one per key; none for linear attention, which has no decay).
+  The RWKV6 bonus u is a per-head parameter shared by every slot and is not counted (as
+  in the paper's model).
 * dense state ``C_state``: p_S * dk * dv bytes per head (p_S = 4 for fp32 state, 2 for
   bf16 state).
 * one log entry ``C_entry``: p_K dk + p_U dv + 4 d_lambda bytes (Eq. 9), with K_log in the
-  activation dtype and U_log fp32 for GDN/KDA, activation dtype for RWKV6.
-* cumulative log-decay ``C_decay``: 4 d_lambda bytes, read and written every DeltaLog step.
+  activation dtype and U_log fp32 for the delta rule (GDN/KDA: computed values), the
+  activation dtype for the others (exact copies of v).
+* cumulative log-decay ``C_decay``: 4 d_lambda bytes, read and written every DeltaLog step
+  (d_lambda = 0 for linear attention: no decay, no snapshots).
 * the output o: fp32, dv values.
 * live-length and index metadata are omitted as lower-order, as the paper does.
 
@@ -28,6 +31,8 @@ Per phase (one head, one token):
 from dataclasses import dataclass
 
 DTYPE_BYTES = {"bf16": 2, "f32": 4}
+DELTA_OPS = ("gdn", "kda")
+PER_KEY_OPS = ("kda", "rwkv6", "gla")
 
 
 @dataclass(frozen=True)
@@ -42,10 +47,11 @@ class HeadTraffic:
 
 def _sizes(op, dk, dv, in_dtype, state_dtype="f32"):
     pin = DTYPE_BYTES[in_dtype]
-    dl = 1 if op == "gdn" else dk
-    common = pin * (2 * dk + dv) + 4 * dl + (4 if op in ("gdn", "kda") else 0)
+    delta = op in DELTA_OPS
+    dl = 0 if op == "linattn" else (dk if op in PER_KEY_OPS else 1)
+    common = pin * (2 * dk + dv) + 4 * dl + (4 if delta else 0)
     state = DTYPE_BYTES[state_dtype] * dk * dv
-    p_u = 4 if op in ("gdn", "kda") else pin
+    p_u = 4 if delta else pin
     entry = pin * dk + p_u * dv + 4 * dl
     decay = 4 * dl
     out = 4 * dv

@@ -2,8 +2,8 @@
 
 The paper measures its kernels on synthetic one-token decode inputs (Sec. 5.1,
 Table 3: H/dk/dv = 32/128/128, bf16 activations, fp32 state); no dataset is
-involved.  This module generates such inputs, reproducibly, for the five workloads
-the library is tested and benchmarked on.  It is the only code shared by the HIP path's
+involved.  This module generates such inputs, reproducibly, for the workloads the
+library is tested and benchmarked on.  It is the only code shared by the HIP path's
 tests/bench and the CPU oracle's tests: it draws random numbers and rounds them to the
 storage dtype, nothing else.
 
@@ -19,6 +19,12 @@ Recipe (also stated in the design doc):
   - KDA: as GDN but lambda = -softplus(z)/16 per key (so alpha = exp(lambda)).
   - RWKV6: r, k, v ~ N(0,1) unnormalised; lambda = log(w) = -exp(-0.5 + 0.5 z) per key;
     no beta; bonus u ~ N(0, 0.1) of shape [H, dk], drawn once.
+  - Linear attention: q, k = phi(z) / |phi(z)| with the positive feature map
+    phi = elu + 1; v ~ N(0,1); no gate (no decay) and no beta are drawn.
+  - RetNet: q, k L2-normalised; v ~ N(0,1); the decay is the fixed per-head
+    gamma_h = 1 - 2^(-5 - 5h/H) (lambda = log gamma_h, the same every step); no gate
+    or beta drawn.
+  - GLA: q, k L2-normalised; v ~ N(0,1); lambda = log sigmoid(z) / 16 per key; no beta.
   - Initial state S0 ~ N(0, 0.02) (standard deviation) for every workload.
 * Rounding: float64 draw -> float32 (round to nearest even) -> bf16 (round to nearest
   even) for bf16 activations.  Gates (lambda) and beta stay float32.  Arrays are returned
@@ -31,6 +37,8 @@ from dataclasses import dataclass, replace
 import numpy as np
 
 ROOT_SEED = 20261202
+PER_KEY_OPS = ("kda", "rwkv6", "gla")
+DELTA_OPS = ("gdn", "kda")
 WARMUP_IDX0 = 10_000
 
 
@@ -38,7 +46,7 @@ WARMUP_IDX0 = 10_000
 class Workload:
     name: str
     cfg: int            # seed component identifying the workload
-    op: str             # "gdn" | "kda" | "rwkv6"
+    op: str             # "gdn" | "kda" | "rwkv6" | "linattn" | "retnet" | "gla"
     B: int              # sequences (state slots)
     H: int              # heads
     dk: int
@@ -55,8 +63,8 @@ class Workload:
 
     @property
     def dl(self):
-        """Width of the log-decay metadata: 1 (head-wise scalar) or dk (per key)."""
-        return 1 if self.op == "gdn" else self.dk
+        """Width of the log-decay metadata: 1 (head-wise scalar, or none) or dk (per key)."""
+        return self.dk if self.op in PER_KEY_OPS else 1
 
     def with_(self, **kw):
         return replace(self, **kw)
@@ -70,7 +78,13 @@ RWKV6_B128 = Workload("rwkv6_b128_h40_d64_m16", 4, "rwkv6", 128, 40, 64, 64, 16,
 GDN_STACK = Workload("gdn_stack24_b256_h32_d128_m16", 5, "gdn", 256, 32, 128, 128, 16, 128,
                      layers=24, staggered=True)
 
-WORKLOADS = {w.name: w for w in (GDN_SMALL, GDN_B64, KDA_B128, RWKV6_B128, GDN_STACK)}
+# The other operators of Table 1, at the GDN / KDA shapes (scalar / per-key decay).
+LINATTN_B64 = Workload("linattn_b64_h32_d128_m16", 6, "linattn", 64, 32, 128, 128, 16, 256)
+RETNET_B64 = Workload("retnet_b64_h32_d128_m16", 7, "retnet", 64, 32, 128, 128, 16, 256)
+GLA_B128 = Workload("gla_b128_h32_d128_m16", 8, "gla", 128, 32, 128, 128, 16, 256)
+
+WORKLOADS = {w.name: w for w in (GDN_SMALL, GDN_B64, KDA_B128, RWKV6_B128, GDN_STACK,
+                                 LINATTN_B64, RETNET_B64, GLA_B128)}
 
 
 def kda_with_merge_interval(M):
@@ -120,11 +134,21 @@ def initial_state(w, layer=0, slots=None):
     return out
 
 
+def _elu1(x):
+    return np.where(x > 0, x + 1.0, np.exp(np.minimum(x, 0.0)))
+
+
+def retnet_log_decay(H):
+    """RetNet's fixed multi-scale decays, one per head: gamma_h = 1 - 2^(-5 - 5h/H)."""
+    return np.log1p(-(2.0 ** (-5.0 - 5.0 * np.arange(H) / H)))
+
+
 def step_inputs(w, t, layer=0, warmup=None):
     """Token inputs for decode step ``t`` (or warm-up step ``warmup``) of all B slots.
 
     Returns a dict of float32 arrays: q [B,H,dk] (r for RWKV6), k [B,H,dk], v [B,H,dv],
-    lam [B,H] (GDN) or [B,H,dk], beta [B,H] (None for RWKV6).
+    lam [B,H] (GDN, RetNet) or [B,H,dk] (KDA, RWKV6, GLA) or None (linear attention),
+    beta [B,H] (delta rule only, else None).
     """
     idx = t if warmup is None else WARMUP_IDX0 + warmup
     g = _rng(w, layer, 1, idx)
@@ -132,7 +156,9 @@ def step_inputs(w, t, layer=0, warmup=None):
     q = g.standard_normal((B, H, dk))
     k = g.standard_normal((B, H, dk))
     v = g.standard_normal((B, H, dv))
-    gate = g.standard_normal((B, H) if w.op == "gdn" else (B, H, dk))
+    beta = None
+    if w.op in ("gdn", "kda", "rwkv6", "gla"):
+        gate = g.standard_normal((B, H) if w.op == "gdn" else (B, H, dk))
     if w.op == "gdn":
         q, k = _l2norm(q), _l2norm(k)
         lam = np.log(_sigmoid(3.0 + 0.5 * gate))
@@ -143,14 +169,22 @@ def step_inputs(w, t, layer=0, warmup=None):
         beta = _sigmoid(g.standard_normal((B, H)))
     elif w.op == "rwkv6":
         lam = -np.exp(-0.5 + 0.5 * gate)
-        beta = None
+    elif w.op == "linattn":
+        q, k = _l2norm(_elu1(q)), _l2norm(_elu1(k))     # positive feature map phi
+        lam = None
+    elif w.op == "retnet":
+        q, k = _l2norm(q), _l2norm(k)
+        lam = np.broadcast_to(retnet_log_decay(H), (B, H))
+    elif w.op == "gla":
+        q, k = _l2norm(q), _l2norm(k)
+        lam = -_softplus(-gate) / 16.0                  # log sigmoid(gate) / 16
     else:
         raise ValueError(w.op)
     return {
         "q": _store(q, w.in_dtype),
         "k": _store(k, w.in_dtype),
         "v": _store(v, w.in_dtype),
-        "lam": lam.astype(np.float32),
+        "lam": None if lam is None else np.ascontiguousarray(lam, dtype=np.float32),
         "beta": None if beta is None else beta.astype(np.float32),
     }
 

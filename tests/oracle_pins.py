@@ -34,13 +34,21 @@ def small_workload(op, N=3, d=8, M=4, steps=12, dk=None, dv=None, in_dtype="f32"
     return W.Workload(f"tiny_{op}", cfg, op, N, 1, dk, dv, M, steps, in_dtype=in_dtype)
 
 
+SCALAR_DECAY_OPS = ("gdn", "retnet", "linattn")   # lambda is one value per head
+DELTA_OPS = ("gdn", "kda")
+
+
 def tiny_inputs(w):
-    """(S0 [N,dk,dv], list of per-step dicts with [N,...] arrays, u [N,dk] or None)."""
+    """(S0 [N,dk,dv], list of per-step dicts with [N,...] arrays, u [N,dk] or None).
+    Linear attention has no decay; its lambda is given as zeros [N]."""
     S0 = W.initial_state(w)[:, 0].astype(np.float64) * 25.0   # O(0.5) entries
     steps = []
     for t in range(w.steps):
         x = W.step_inputs(w, t)
-        steps.append({k: (None if a is None else a[:, 0].astype(np.float64)) for k, a in x.items()})
+        st = {k: (None if a is None else a[:, 0].astype(np.float64)) for k, a in x.items()}
+        if st["lam"] is None:
+            st["lam"] = np.zeros(w.B)
+        steps.append(st)
     u = W.bonus(w)
     u = None if u is None else np.broadcast_to(u[0], (w.B, w.dk)).astype(np.float64)
     return S0, steps, u
@@ -55,9 +63,14 @@ def _bf_step_fraction(op, S, q, k, v, beta, g, u):
                    S_ij <- S'_ij + k_i b_j;  o_j = sum_i q_i S_ij  (post-update)
       RWKV6:       o_j = sum_i r_i S_ij + (sum_i r_i u_i k_i) v_j  (pre-update + bonus)
                    S_ij <- g_i S_ij + k_i v_j
+      additive:    S_ij <- g_i S_ij + k_i v_j;  o_j = sum_i q_i S_ij  (post-update)
+                   (linear attention g = 1, RetNet g_0 = g_1, GLA per key)
     """
     n = 2
-    if op in ("gdn", "kda"):
+    if op in ("linattn", "retnet", "gla"):
+        Sn = [[g[i] * S[i][j] + k[i] * v[j] for j in range(n)] for i in range(n)]
+        o = [q[0] * Sn[0][j] + q[1] * Sn[1][j] for j in range(n)]
+    elif op in ("gdn", "kda"):
         Sd = [[g[i] * S[i][j] for j in range(n)] for i in range(n)]
         c = [k[0] * Sd[0][j] + k[1] * Sd[1][j] for j in range(n)]
         b = [beta * (v[j] - c[j]) for j in range(n)]
@@ -84,10 +97,15 @@ def pin_bruteforce_2x2(step, op):
     u = [Fr(1, 5), Fr(-2, 5)]
     Sf = np.array([[float(x) for x in row] for row in S])[None]
     for t, st in enumerate(seq):
-        g = st["g"] if op != "gdn" else [st["g"][0], st["g"][0]]
+        if op == "linattn":
+            g = [Fr(1), Fr(1)]
+        elif op in SCALAR_DECAY_OPS:
+            g = [st["g"][0], st["g"][0]]
+        else:
+            g = st["g"]
         S, o = _bf_step_fraction(op, S, st["q"], st["k"], st["v"], st["beta"], g, u)
         f = lambda xs: np.array([float(x) for x in xs])[None]
-        lam = np.log(f(g)) if op != "gdn" else np.log(np.array([float(g[0])]))
+        lam = np.log(np.array([float(g[0])])) if op in SCALAR_DECAY_OPS else np.log(f(g))
         Sf, of = step(op, Sf, f(st["q"]), f(st["k"]), f(st["v"]),
                       np.array([float(st["beta"])]), lam,
                       f(u) if op == "rwkv6" else None)
@@ -96,31 +114,37 @@ def pin_bruteforce_2x2(step, op):
         _close(of, f(o), 1e-13, f"{op} 2x2 output step {t}")
 
 
+def _no_write(op, st):
+    """(k, beta) of a step that writes nothing: beta = 0 (delta rule) or k = 0."""
+    if op in DELTA_OPS:
+        return st["k"], np.zeros_like(st["beta"])
+    return np.zeros_like(st["k"]), None
+
+
 def pin_identity(step, op):
-    """beta = 0, lambda = 0 (delta rule) or k = 0, lambda = 0 (RWKV6): S unchanged, o = S^T q."""
+    """No write (beta = 0 for the delta rule, else k = 0) and lambda = 0: S unchanged and
+    o = S^T q."""
     w = small_workload(op)
     S0, steps, u = tiny_inputs(w)
     st = steps[0]
     lam = np.zeros_like(st["lam"])
-    k = np.zeros_like(st["k"]) if op == "rwkv6" else st["k"]
-    beta = np.zeros_like(st["beta"]) if op != "rwkv6" else None
+    k, beta = _no_write(op, st)
     S1, o = step(op, S0, st["q"], k, st["v"], beta, lam, u)
     _close(S1, S0, 0.0, f"{op} identity state")
     _close(o, np.einsum("ni,nij->nj", st["q"], S0), 1e-14, f"{op} identity output")
 
 
 def pin_decay_only(step, op):
-    """n steps with no write (beta = 0, or k = 0 for RWKV6): S_n = diag(exp(sum lambda)) S_0."""
+    """n steps with no write: S_n = diag(exp(sum lambda)) S_0 (S_0 for linear attention)."""
     w = small_workload(op, steps=5)
     S0, steps, u = tiny_inputs(w)
     S = S0
     tot = np.zeros_like(steps[0]["lam"])
     for st in steps:
-        k = np.zeros_like(st["k"]) if op == "rwkv6" else st["k"]
-        beta = np.zeros_like(st["beta"]) if op != "rwkv6" else None
+        k, beta = _no_write(op, st)
         S, _ = step(op, S, st["q"], k, st["v"], beta, st["lam"], u)
         tot = tot + st["lam"]
-    rows = np.exp(tot)[:, None, None] if op == "gdn" else np.exp(tot)[:, :, None]
+    rows = np.exp(tot)[:, None, None] if op in SCALAR_DECAY_OPS else np.exp(tot)[:, :, None]
     _close(S, rows * S0, 1e-14, f"{op} decay-only closed form")
 
 
@@ -201,6 +225,71 @@ def pin_rwkv6_bonus(step):
     _close(o, np.sum(r * u * k) * v, 1e-14, "rwkv6 bonus")
 
 
+def _sequence(op, T, d=8, seed=21):
+    """S0 [1,d,d] and a T-step sequence of the op's inputs (shared generator)."""
+    w = small_workload(op, N=1, d=d, steps=T, cfg=seed)
+    S0, steps, _ = tiny_inputs(w)
+    Q = np.stack([st["q"][0] for st in steps])
+    K = np.stack([st["k"][0] for st in steps])
+    V = np.stack([st["v"][0] for st in steps])
+    return S0, steps, Q, K, V
+
+
+def _run(step, op, S0, steps):
+    S, outs = S0, []
+    for st in steps:
+        S, o = step(op, S, st["q"], st["k"], st["v"], None, st["lam"], None)
+        outs.append(o[0])
+    return S[0], np.stack(outs)
+
+
+def pin_linear_attention_matrix_form(step):
+    """Causal linear attention (Eq. 1) in matrix form: O = Q S0 + tril(Q K^T) V, and the
+    final state is S0 + K^T V."""
+    S0, steps, Q, K, V = _sequence("linattn", 9)
+    S, O = _run(step, "linattn", S0, steps)
+    _close(O, Q @ S0[0] + np.tril(Q @ K.T) @ V, 1e-13, "linear attention outputs")
+    _close(S, S0[0] + K.T @ V, 1e-13, "linear attention state")
+
+
+def pin_retnet_parallel_form(step):
+    """RetNet's parallel retention with a fixed gamma: o_n = gamma^(n+1) q_n^T S0 +
+    sum_{m<=n} gamma^(n-m) (q_n . k_m) v_m, i.e. O = (Q K^T * Dg) V + diag(gamma^(n+1)) Q S0."""
+    S0, steps, Q, K, V = _sequence("retnet", 10)
+    gamma = 0.9
+    for st in steps:
+        st["lam"] = np.full(1, np.log(gamma))
+    S, O = _run(step, "retnet", S0, steps)
+    n = np.arange(len(steps))
+    Dg = np.where(n[:, None] >= n[None, :], gamma ** (n[:, None] - n[None, :]), 0.0)
+    ref = (Q @ K.T * Dg) @ V + (gamma ** (n + 1))[:, None] * (Q @ S0[0])
+    _close(O, ref, 1e-13, "retnet parallel form")
+
+
+def pin_gla_parallel_form(step):
+    """Gated linear attention in parallel form: with cumulative gates b_t = prod_{r<=t}
+    exp(lambda_r) (per key), o_t = (q_t * b_t)^T S0 + sum_{s<=t} ((q_t * b_t) . (k_s / b_s)) v_s."""
+    S0, steps, Q, K, V = _sequence("gla", 10)
+    S, O = _run(step, "gla", S0, steps)
+    Bc = np.exp(np.cumsum(np.stack([st["lam"][0] for st in steps]), axis=0))
+    Qb, Kb = Q * Bc, K / Bc
+    _close(O, np.tril(Qb @ Kb.T) @ V + Qb @ S0[0], 1e-12, "gla parallel form")
+    _close(S, Bc[-1][:, None] * S0[0] + Kb.T @ V * Bc[-1][:, None], 1e-12, "gla state")
+
+
+def pin_gla_equal_gates_is_retnet(step):
+    """GLA whose per-key gates are all equal is RetNet with that scalar decay."""
+    S0, steps, _, _, _ = _sequence("gla", 6)
+    Sg = Sr = S0
+    for st in steps:
+        lam_s = st["lam"][:, :1]
+        Sg, og = step("gla", Sg, st["q"], st["k"], st["v"], None,
+                      np.broadcast_to(lam_s, st["lam"].shape), None)
+        Sr, o_r = step("retnet", Sr, st["q"], st["k"], st["v"], None, lam_s[:, 0], None)
+        _close(Sg, Sr, 1e-15, "gla==retnet state")
+        _close(og, o_r, 1e-15, "gla==retnet output")
+
+
 # --------------------------------------------------------------------------- model
 def _eager_seq(step, op, S0, steps, u):
     S = S0
@@ -278,7 +367,7 @@ def pin_model_merge_is_gemm(Model, op):
     dk = S0.shape[1]
     e = np.exp(np.broadcast_to(ell_new, (w.B, dk)))
     Kt = np.exp(np.broadcast_to(ell_new[:, None, :] - Lam, (w.B, M - 1, dk))) * K
-    if op == "rwkv6":
+    if op not in DELTA_OPS:
         a, b = st["k"], st["v"]
     else:
         S_dec = e[:, :, None] * Sbar + np.matmul(Kt.transpose(0, 2, 1), U)

@@ -72,10 +72,43 @@ def _mut_rwkv6(kind):
     return step
 
 
+def _mut_additive(kind):
+    def step(op, S, q, k, v, beta, lam, u):
+        if op not in eager.ADDITIVE_OPS:
+            return eager.eager_step(op, S, q, k, v, beta, lam, u=u)
+        S, q, k, v = (np.asarray(x, dtype=np.float64) for x in (S, q, k, v))
+        if op == "linattn":
+            rows = np.ones(S.shape[:-1] + (1,))
+        else:
+            rows = eager.row_decay(lam, S.shape[-2], op == "gla")
+        Sd = rows * S
+        if kind == "ignore_decay":
+            Sd = S
+        if kind == "column_decay":
+            Sd = np.swapaxes(rows, -1, -2) * S
+        outer = k[..., :, None] * v[..., None, :]
+        if kind == "outer_transposed":
+            outer = np.swapaxes(outer, -1, -2)
+        S_new = Sd + outer
+        if kind == "decay_after_write":
+            S_new = rows * (S + outer)
+        if kind == "drop_state":
+            S_new = outer
+        o = _ein(q, S_new)
+        if kind == "pre_update_output":
+            o = _ein(q, Sd)
+        if kind == "transposed_readout":
+            o = np.einsum("...i,...ji->...j", q, S_new)
+        return S_new, o
+    return step
+
+
 DELTA_MUTANTS = ["column_decay", "negated_decay", "undecayed", "correction_with_q", "drop_beta",
                  "sign", "drop_correction", "outer_transposed", "pre_update_output",
                  "transposed_readout"]
 RWKV6_MUTANTS = ["bonus_without_u", "no_bonus", "post_update_readout", "undecayed_write"]
+ADDITIVE_MUTANTS = ["ignore_decay", "column_decay", "outer_transposed", "decay_after_write",
+                    "drop_state", "pre_update_output", "transposed_readout"]
 
 
 def _eager_pins(step, ops):
@@ -83,12 +116,19 @@ def _eager_pins(step, ops):
         yield lambda op=op: P.pin_bruteforce_2x2(step, op)
         yield lambda op=op: P.pin_identity(step, op)
         yield lambda op=op: P.pin_decay_only(step, op)
-        if op != "rwkv6":
+        if op in ("gdn", "kda"):
             yield lambda op=op: P.pin_delta_write(step, op)
             yield lambda op=op: P.pin_published_delta_rule(step, op)
     if "rwkv6" in ops:
         yield lambda: P.pin_rwkv6_linear_attention(step)
         yield lambda: P.pin_rwkv6_bonus(step)
+    if "linattn" in ops:
+        yield lambda: P.pin_linear_attention_matrix_form(step)
+    if "retnet" in ops:
+        yield lambda: P.pin_retnet_parallel_form(step)
+    if "gla" in ops:
+        yield lambda: P.pin_gla_parallel_form(step)
+        yield lambda: P.pin_gla_equal_gates_is_retnet(step)
 
 
 def _caught(pins):
@@ -111,6 +151,16 @@ def test_eager_delta_rule_mutant_is_caught(op, kind):
 @pytest.mark.parametrize("kind", RWKV6_MUTANTS)
 def test_eager_rwkv6_mutant_is_caught(kind):
     assert _caught(_eager_pins(_mut_rwkv6(kind), ("rwkv6",))), f"rwkv6 mutant {kind} not caught"
+
+
+@pytest.mark.parametrize("kind", ADDITIVE_MUTANTS)
+@pytest.mark.parametrize("op", ("linattn", "retnet", "gla"))
+def test_eager_additive_mutant_is_caught(op, kind):
+    if op == "linattn" and kind in ("ignore_decay", "column_decay", "decay_after_write"):
+        pytest.skip("linear attention has no decay: not a mistake for it")
+    if op == "retnet" and kind == "column_decay":
+        pytest.skip("a scalar decay scales rows and columns alike: not a mistake for RetNet")
+    assert _caught(_eager_pins(_mut_additive(kind), (op,))), f"{op} mutant {kind} not caught"
 
 
 # ------------------------------------------------------------------ model mutants
@@ -180,9 +230,15 @@ def _real_step(op, S, q, k, v, beta, lam, u):
     return eager.eager_step(op, S, q, k, v, beta, lam, u=u)
 
 
+DECAY_BOOKKEEPING = (SnapshotBeforeDecay, NoResetAtMerge, DecaySumNotDifference,
+                     EllNotAdvancedOnAppend)
+
+
 @pytest.mark.parametrize("Model", MODEL_MUTANTS, ids=lambda c: c.__name__)
-@pytest.mark.parametrize("op", ("gdn", "kda", "rwkv6"))
+@pytest.mark.parametrize("op", eager.OPS)
 def test_model_mutant_is_caught(op, Model):
+    if op == "linattn" and Model in DECAY_BOOKKEEPING:
+        pytest.skip("linear attention's log-decay is identically zero: not a mistake for it")
     pins = [lambda M=M: P.pin_model_matches_eager(Model, _real_step, op, M) for M in (2, 3, 8)]
     pins.append(lambda: P.pin_model_merge_is_gemm(Model, op))
     pins.append(lambda: P.pin_model_flush_and_readout(Model, _real_step, op))

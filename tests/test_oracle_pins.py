@@ -7,7 +7,7 @@ from oracle.deltalog_model import DeltaLogModel
 
 import oracle_pins as P
 
-OPS = ("gdn", "kda", "rwkv6")
+OPS = eager.OPS
 
 
 def step(op, S, q, k, v, beta, lam, u):
@@ -49,6 +49,22 @@ def test_rwkv6_reduces_to_linear_attention():
 
 def test_rwkv6_bonus_term():
     P.pin_rwkv6_bonus(step)
+
+
+def test_linear_attention_matrix_form():
+    P.pin_linear_attention_matrix_form(step)
+
+
+def test_retnet_parallel_retention():
+    P.pin_retnet_parallel_form(step)
+
+
+def test_gla_parallel_form():
+    P.pin_gla_parallel_form(step)
+
+
+def test_gla_with_equal_gates_is_retnet():
+    P.pin_gla_equal_gates_is_retnet(step)
 
 
 @pytest.mark.parametrize("op", OPS)

@@ -21,13 +21,15 @@ def test_step_inputs_shapes_and_determinism(w):
     a, b = W.step_inputs(w, 3), W.step_inputs(w, 3)
     for key in a:
         if a[key] is None:
-            assert w.op == "rwkv6" and key == "beta"
+            assert (key == "beta" and w.op not in ("gdn", "kda")) or \
+                (key == "lam" and w.op == "linattn")
             continue
         np.testing.assert_array_equal(a[key], b[key])
         assert a[key].dtype == np.float32
     assert a["q"].shape == (w.B, w.H, w.dk) and a["v"].shape == (w.B, w.H, w.dv)
-    assert a["lam"].shape == ((w.B, w.H) if w.op == "gdn" else (w.B, w.H, w.dk))
-    assert np.all(a["lam"] <= 0.0)
+    if w.op != "linattn":
+        assert a["lam"].shape == ((w.B, w.H) if w.dl == 1 else (w.B, w.H, w.dk))
+        assert np.all(a["lam"] <= 0.0)
     if w.in_dtype == "bf16":
         for key in ("q", "k", "v"):
             np.testing.assert_array_equal(W.round_bf16(a[key]), a[key])
@@ -55,6 +57,14 @@ def test_gate_distributions():
     r = W.step_inputs(W.RWKV6_B128.with_(B=8), 0)
     w6 = np.exp(r["lam"].astype(np.float64))
     assert 0.5 < w6.mean() < 0.6
+    gl = W.step_inputs(W.GLA_B128.with_(B=8), 0)
+    assert abs(np.mean(16.0 * gl["lam"]) + 0.806) < 0.02   # E[log sigmoid(N(0,1))] ~ -0.806
+    rn = W.step_inputs(W.RETNET_B64.with_(B=2), 5)
+    gamma = np.exp(rn["lam"][0].astype(np.float64))
+    np.testing.assert_allclose(1.0 - gamma, 2.0 ** (-5.0 - 5.0 * np.arange(32) / 32), rtol=1e-5)
+    assert np.array_equal(rn["lam"], W.step_inputs(W.RETNET_B64.with_(B=2), 9)["lam"])
+    la = W.step_inputs(W.LINATTN_B64.with_(B=2), 0)
+    assert np.all(la["q"] > 0) and np.all(la["k"] > 0)     # positive feature map
 
 
 def test_staggered_warmup_reaches_offsets():
