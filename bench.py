@@ -53,6 +53,9 @@ def workloads():
         "kda_b128_h32_d128_m16": (W.kda_with_merge_interval(16), 4),
         "kda_b128_h32_d128_m32": (W.kda_with_merge_interval(32), 4),
         "rwkv6_b128_h40_d64_m16": (W.RWKV6_B128, 12),
+        "linattn_b64_h32_d128_m16": (W.LINATTN_B64, 8),
+        "retnet_b64_h32_d128_m16": (W.RETNET_B64, 8),
+        "gla_b128_h32_d128_m16": (W.GLA_B128, 4),
         "gdn_stack24_b256_h32_d128_m16": (W.GDN_STACK, 24),
     }
 
@@ -151,7 +154,7 @@ def cpu_baseline(w, budget_s):
     steps = 0
     while True:
         x = xs[steps % len(xs)]
-        S, _ = OE.eager_step(w.op, S, x["q"], x["k"], x["v"], x["beta"], x["lam"], u=u)
+        S, _ = OE.eager_step(w.op, S, x["q"], x["k"], x["v"], x["beta"], x.get("lam"), u=u)
         steps += 1
         el = time.perf_counter() - wall0
         if el >= budget_s or steps >= 256:
@@ -435,7 +438,8 @@ def main():
 
     traffic, traffic_src = counter_traffic(profile_key(args.workload, sd))
     state_mib = heads * w.dk * w.dv * (2 if sd == "bf16" else 4) / 2**20
-    kname = {"gdn": "GDN", "kda": "KDA", "rwkv6": "RWKV6"}[w.op]
+    kname = {"gdn": "GDN", "kda": "KDA", "rwkv6": "RWKV6", "linattn": "LinearAttention",
+             "retnet": "RetNet", "gla": "GLA"}[w.op]
     res = {
         "metric": METRIC,
         "value": round(dl_tok, 1),

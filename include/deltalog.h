@@ -66,14 +66,28 @@ typedef enum {
   DL_E_VERSION = -7      /* desc->abi_version != DL_ABI_VERSION                         */
 } dl_status;
 
-typedef enum { DL_OP_GDN = 0, DL_OP_KDA = 1, DL_OP_RWKV6 = 2 } dl_op;
+typedef enum {
+  DL_OP_GDN = 0,
+  DL_OP_KDA = 1,
+  DL_OP_RWKV6 = 2,
+  DL_OP_LINATTN = 3,
+  DL_OP_RETNET = 4,
+  DL_OP_GLA = 5
+} dl_op;
 typedef enum { DL_F32 = 0, DL_BF16 = 1 } dl_dtype;
 
 /* Problem description (host memory, read during the call only).
- * Operators (Table 1): GDN = head-wise scalar decay with the delta-rule pair
- * (k, beta (v - k^T D(lambda) S)); KDA = per-key decay with the same pair;
- * RWKV6 = per-key decay with the pair (k, v) and the bonus readout
- * o = r^T (S_{t-1} + diag(u) k v^T). */
+ * Operators (Table 1, Eq. 3):
+ *   GDN     head-wise scalar decay, delta-rule pair (k, beta (v - k^T D(lambda) S)),
+ *           post-update readout o = q^T S_t;
+ *   KDA     per-key decay, the same pair and readout;
+ *   RWKV6   per-key decay, pair (k, v), bonus readout o = r^T (S_{t-1} + diag(u) k v^T);
+ *   LINATTN no decay, pair (phi(k), v) with phi applied by the caller, o = q^T S_t
+ *           (Eq. 1);
+ *   RETNET  head-wise scalar decay gamma_t = exp(lambda_t), pair (k, v), o = q^T S_t;
+ *   GLA     per-key decay, pair (k, v), o = q^T S_t.
+ * dl (the log-decay width) is dk for KDA, RWKV6 and GLA and 1 for GDN and RetNet;
+ * linear attention has no log-decay and touches none of ell, lam_log or lam. */
 typedef struct {
   int32_t abi_version;    /* must be DL_ABI_VERSION                                      */
   int32_t op;             /* dl_op                                                       */
@@ -83,7 +97,7 @@ typedef struct {
   int32_t merge_interval; /* M in [1, 64]: one merge every M steps (Sec. 3.1); C = M-1   */
   int32_t in_dtype;       /* dl_dtype of q/r, k, v; K_log stores exact copies of k       */
   int32_t u_log_dtype;    /* dl_dtype of U_log: DL_F32 for GDN/KDA (corrected values),   */
-                          /* == in_dtype for RWKV6 (exact copies of v)                   */
+                          /* == in_dtype for the others (exact copies of v)              */
   int32_t state_dtype;    /* dl_dtype of the dense state S: DL_F32, or DL_BF16 (all       */
                           /* arithmetic in fp32, S rounded to bf16 -- nearest even -- on  */
                           /* every store; every other buffer keeps its dtype)            */
@@ -93,9 +107,11 @@ typedef struct {
 typedef struct {
   void*    S;        /* [B,H,dk,dv] state_dtype dense base                               */
   float*   ell;      /* [B,H,dl]    fp32 cumulative log-decay since the last merge       */
+                     /*             (ignored, may be NULL, for LINATTN)                  */
   void*    k_log;    /* [B,H,C,dk]  in_dtype   key-side factors   (may be NULL if C == 0) */
   void*    u_log;    /* [B,H,C,dv]  u_log_dtype value-side factors (may be NULL if C == 0)*/
   float*   lam_log;  /* [B,H,C,dl]  fp32 snapshot of ell per entry (may be NULL if C == 0)*/
+                     /*             (ignored, may be NULL, for LINATTN)                  */
   int32_t* len;      /* [B,H]       live-log length L in [0, C]                          */
   int32_t* err;      /* [1]         sticky device error word (see above); may be NULL    */
 } dl_state;
@@ -105,8 +121,9 @@ typedef struct {
   const void*  q;    /* [n,H,dk] in_dtype: query (the receptance r for RWKV6)            */
   const void*  k;    /* [n,H,dk] in_dtype: key, the key-side factor a_t                  */
   const void*  v;    /* [n,H,dv] in_dtype: value                                         */
-  const float* beta; /* [n,H]    fp32 delta-rule write strength (GDN/KDA); NULL for RWKV6*/
+  const float* beta; /* [n,H]    fp32 delta-rule write strength (GDN/KDA); else ignored  */
   const float* lam;  /* [n,H,dl] fp32 per-step log-decay lambda_t = log(alpha_t) <= 0     */
+                     /*          (ignored, may be NULL, for LINATTN)                     */
   const float* u;    /* [H,dk]   fp32 RWKV6 bonus (per-head parameter); NULL otherwise   */
 } dl_token;
 

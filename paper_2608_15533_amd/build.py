@@ -21,7 +21,8 @@ BUILD_DIR = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libdeltalog.so")
 ARCH = "gfx950"
 
-SOURCES = ["abi.cpp", "dl_gdn.hip", "dl_kda.hip", "dl_rwkv6.hip"]
+SOURCES = ["abi.cpp", "dl_gdn.hip", "dl_kda.hip", "dl_rwkv6.hip", "dl_linattn.hip",
+           "dl_retnet.hip", "dl_gla.hip"]
 
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 

@@ -16,10 +16,13 @@ using dl::KParams;
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
+bool is_delta(int op) { return op == DL_OP_GDN || op == DL_OP_KDA; }
+bool has_decay(int op) { return op != DL_OP_LINATTN; }
+
 int check_desc(const dl_desc* d) {
   if (!d) return DL_E_NULL;
   if (d->abi_version != DL_ABI_VERSION) return DL_E_VERSION;
-  if (d->op != DL_OP_GDN && d->op != DL_OP_KDA && d->op != DL_OP_RWKV6) return DL_E_UNSUPPORTED;
+  if (d->op < DL_OP_GDN || d->op > DL_OP_GLA) return DL_E_UNSUPPORTED;
   if ((d->dk != 64 && d->dk != 128) || (d->dv != 64 && d->dv != 128)) return DL_E_UNSUPPORTED;
   if (d->merge_interval < 1 || d->merge_interval > DL_MAX_MERGE_INTERVAL) return DL_E_UNSUPPORTED;
   if (d->num_slots < 1 || d->heads < 1) return DL_E_SHAPE;
@@ -27,10 +30,10 @@ int check_desc(const dl_desc* d) {
   if (int64_t(d->num_slots) * d->heads > int64_t(0x7fffffff)) return DL_E_SHAPE;
   if (d->in_dtype != DL_F32 && d->in_dtype != DL_BF16) return DL_E_DTYPE;
   if (d->state_dtype != DL_F32 && d->state_dtype != DL_BF16) return DL_E_DTYPE;
-  if (d->op == DL_OP_RWKV6) {
-    if (d->u_log_dtype != d->in_dtype) return DL_E_DTYPE;   // U_log holds copies of v
-  } else {
+  if (is_delta(d->op)) {
     if (d->u_log_dtype != DL_F32) return DL_E_DTYPE;        // U_log holds computed b
+  } else {
+    if (d->u_log_dtype != d->in_dtype) return DL_E_DTYPE;   // U_log holds copies of v
   }
   return DL_OK;
 }
@@ -44,23 +47,30 @@ int check_rows(const dl_desc* d, const int32_t* slots, int32_t n) {
 }
 
 int check_token(const dl_desc* d, const dl_token* t) {
-  if (!t || !t->q || !t->k || !t->v || !t->lam) return DL_E_NULL;
+  if (!t || !t->q || !t->k || !t->v) return DL_E_NULL;
+  if (has_decay(d->op)) {
+    if (!t->lam) return DL_E_NULL;
+    if (!aligned(t->lam, 4)) return DL_E_ALIGN;
+  }
   if (d->op == DL_OP_RWKV6) {
     if (!t->u) return DL_E_NULL;
     if (!aligned(t->u, 4)) return DL_E_ALIGN;
-  } else {
+  }
+  if (is_delta(d->op)) {
     if (!t->beta) return DL_E_NULL;
     if (!aligned(t->beta, 4)) return DL_E_ALIGN;
   }
   if (!aligned(t->q, 16) || !aligned(t->k, 16) || !aligned(t->v, 16)) return DL_E_ALIGN;
-  if (!aligned(t->lam, 4)) return DL_E_ALIGN;
   return DL_OK;
 }
 
 int check_state(const dl_desc* d, const dl_state* s) {
-  if (!s || !s->S || !s->ell || !s->len) return DL_E_NULL;
-  if (d->merge_interval > 1 && (!s->k_log || !s->u_log || !s->lam_log)) return DL_E_NULL;
-  if (!aligned(s->S, 16) || !aligned(s->ell, 4) || !aligned(s->len, 4)) return DL_E_ALIGN;
+  const bool decay = has_decay(d->op);
+  if (!s || !s->S || !s->len || (decay && !s->ell)) return DL_E_NULL;
+  if (d->merge_interval > 1 && (!s->k_log || !s->u_log)) return DL_E_NULL;
+  if (d->merge_interval > 1 && decay && !s->lam_log) return DL_E_NULL;
+  if (!aligned(s->S, 16) || !aligned(s->len, 4)) return DL_E_ALIGN;
+  if (s->ell && !aligned(s->ell, 4)) return DL_E_ALIGN;
   if (s->k_log && !aligned(s->k_log, 16)) return DL_E_ALIGN;
   if (s->u_log && !aligned(s->u_log, 16)) return DL_E_ALIGN;
   if (s->lam_log && !aligned(s->lam_log, 4)) return DL_E_ALIGN;
@@ -106,6 +116,9 @@ int launch(const dl_desc* d, int mode, const KParams& p, hipStream_t stream) {
     case DL_OP_GDN: e = dl::launch_gdn(mode, d->dk, d->dv, bf16, sbf16, p, stream); break;
     case DL_OP_KDA: e = dl::launch_kda(mode, d->dk, d->dv, bf16, sbf16, p, stream); break;
     case DL_OP_RWKV6: e = dl::launch_rwkv6(mode, d->dk, d->dv, bf16, sbf16, p, stream); break;
+    case DL_OP_LINATTN: e = dl::launch_linattn(mode, d->dk, d->dv, bf16, sbf16, p, stream); break;
+    case DL_OP_RETNET: e = dl::launch_retnet(mode, d->dk, d->dv, bf16, sbf16, p, stream); break;
+    case DL_OP_GLA: e = dl::launch_gla(mode, d->dk, d->dv, bf16, sbf16, p, stream); break;
   }
   return e == hipSuccess ? DL_OK : DL_E_HIP;
 }

@@ -9,13 +9,20 @@
 
 namespace dl {
 
-enum OpId { OP_GDN = DL_OP_GDN, OP_KDA = DL_OP_KDA, OP_RWKV6 = DL_OP_RWKV6 };
+enum OpId {
+  OP_GDN = DL_OP_GDN,
+  OP_KDA = DL_OP_KDA,
+  OP_RWKV6 = DL_OP_RWKV6,
+  OP_LINATTN = DL_OP_LINATTN,
+  OP_RETNET = DL_OP_RETNET,
+  OP_GLA = DL_OP_GLA
+};
 enum ModeId { M_EAGER = 0, M_STEP = 1, M_MERGE = 2, M_FLUSH = 3, M_READOUT = 4 };
 
 // Everything a kernel needs, passed by value (all pointers are device pointers).
 struct KParams {
   void* S;               // [B,H,dk,dv] dense base (or the eager dense state), fp32 or bf16
-  float* ell;            // [B,H,dl]
+  float* ell;            // [B,H,dl] (unused by linear attention)
   void* k_log;           // [B,H,C,dk]
   void* u_log;           // [B,H,C,dv]
   float* lam_log;        // [B,H,C,dl]
@@ -40,5 +47,11 @@ hipError_t launch_kda(int mode, int dk, int dv, bool bf16, bool state_bf16, cons
                       hipStream_t s);
 hipError_t launch_rwkv6(int mode, int dk, int dv, bool bf16, bool state_bf16, const KParams& p,
                         hipStream_t s);
+hipError_t launch_linattn(int mode, int dk, int dv, bool bf16, bool state_bf16, const KParams& p,
+                          hipStream_t s);
+hipError_t launch_retnet(int mode, int dk, int dv, bool bf16, bool state_bf16, const KParams& p,
+                         hipStream_t s);
+hipError_t launch_gla(int mode, int dk, int dv, bool bf16, bool state_bf16, const KParams& p,
+                      hipStream_t s);
 
 }  // namespace dl

@@ -1,16 +1,17 @@
 // DeltaLog decode kernels for gfx950 (CDNA4, wave64).
 //
-// One workgroup owns one (slot, head) state: a dk x dv fp32 matrix (64 KiB at 128x128).
+// One workgroup owns one (slot, head) state: a dk x dv matrix (64 KiB at 128x128 fp32).
 // Thread layout: NCG = dv/4 column groups (one float4 column slice each) times
 // NRG = dk/RPT row groups; every thread keeps RPT rows x 4 columns of the state in
 // registers (rows rg, rg+NRG, ..., so one wave-wide float4 load covers whole
-// consecutive rows, 1 KiB contiguous).  RPT = 16, or 8 for 64 x 64 heads.  The state is read from HBM exactly once
-// per step and, when the step materialises (merge / eager / flush), written back
-// exactly once from the same registers -- the read, the key-dimension reductions
-// and the write never leave the workgroup.  Because one workgroup owns all of a
-// head's value columns, the replay coefficients are computed once per (slot, head)
-// and the shared log metadata (K_log[L], Lam_log[L], ell, L) has a single writer
-// without any cross-workgroup finalisation (the ownership problem of Sec. 3.3).
+// consecutive rows, 1 KiB contiguous).  RPT = 16, or 8 for 64 x 64 heads.  The state
+// is read from HBM exactly once per step and, when the step materialises (merge /
+// eager / flush), written back exactly once from the same registers -- the read, the
+// key-dimension reductions and the write never leave the workgroup.  Because one
+// workgroup owns all of a head's value columns, the replay coefficients are computed
+// once per (slot, head) and the shared log metadata (K_log[L], Lam_log[L], ell, L) has
+// a single writer without any cross-workgroup finalisation (the ownership problem of
+// Sec. 3.3).
 //
 // Modes (one template per mode; the per-slot append/merge branch of Alg. 1 is taken
 // on the device from that slot's live length):
@@ -22,17 +23,22 @@
 //
 // Per (slot, head) and step the arithmetic is (l' = ell + lambda):
 //   replay coefficient of entry i for a vector x:  g_i(x) = sum_r e^(l_r - Lam_i,r) x_r K_i,r
-//   base readout:   sum_r e^(l_r) x_r S_r,:      (l = l' for GDN/KDA, ell for RWKV6)
+//   base readout:   sum_r e^(l_r) x_r S_r,:      (l = ell for RWKV6, l' otherwise)
 //   correction c = base(k) + sum_i g_i(k) U_i ;  b = beta (v - c)             (GDN/KDA)
-//   output     o = base(q) + sum_i g_i(q) U_i + (q.k) b                       (GDN/KDA)
+//              b = v                             (RWKV6, linear attention, RetNet, GLA)
+//   output     o = base(q) + sum_i g_i(q) U_i + (q.k) b    (post-update: all but RWKV6)
 //              o = base(r) + sum_i g_i(r) U_i + (r.(u*k)) v                   (RWKV6)
 //   merge      S <- diag(e^l') S + sum_i diag(e^(l'-Lam_i)) K_i U_i^T + k b^T  (Eq. 6)
+// Linear attention has no decay: every e^(.) above is 1 and ell, Lam_log and lambda are
+// never touched.
 // Every decay factor is evaluated as exp of a log-decay *difference* (<= 0 in normal
 // use), never as a product of exp(l') and exp(-Lam_i).
 #pragma once
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include <type_traits>
 
 #include "dl_internal.h"
 
@@ -264,6 +270,15 @@ constexpr int rows_per_thread(int dk, int dv) {
 }
 constexpr int threads_per_head(int dk, int dv) { return (dv / 4) * (dk / rows_per_thread(dk, dv)); }
 
+// What distinguishes the operators of Table 1 inside the kernel.
+template <int OP>
+struct OpTraits {
+  static constexpr bool DELTA = OP == OP_GDN || OP == OP_KDA;   // b = beta (v - correction)
+  static constexpr bool PER_KEY = OP == OP_KDA || OP == OP_RWKV6 || OP == OP_GLA;
+  static constexpr bool DECAY = OP != OP_LINATTN;               // linear attention: none
+  static constexpr bool BONUS = OP == OP_RWKV6;   // pre-update readout plus r^T diag(u) k v^T
+};
+
 template <int OP, int DK, int DV, int MODE>
 struct Cfg {
   static constexpr int RPT = rows_per_thread(DK, DV);   // state rows held per thread
@@ -271,13 +286,15 @@ struct Cfg {
   static constexpr int NRG = DK / RPT;           // row groups
   static constexpr int NT = NCG * NRG;           // threads per workgroup
   static constexpr int NW = NT / 64;             // waves per workgroup
-  static constexpr int DL = (OP == OP_GDN) ? 1 : DK;   // log-decay width
+  static constexpr int DL = OpTraits<OP>::PER_KEY ? DK : 1;   // log-decay width
   static constexpr int EPP = 16;                 // log entries per coefficient pass
   static constexpr int LPE = NT / EPP;           // lanes per log entry (coefficient pass)
   static constexpr int RPL = DK / LPE;           // key rows per lane (coefficient pass)
   static constexpr int CH = 16;                  // log entries staged per merge chunk
   static constexpr int KTS = CH + 4;             // LDS row stride of the staged K~ chunk
-  static constexpr bool DELTA = OP != OP_RWKV6;
+  static constexpr bool DELTA = OpTraits<OP>::DELTA;
+  static constexpr bool DECAY = OpTraits<OP>::DECAY;
+  static constexpr bool BONUS = OpTraits<OP>::BONUS;
   static constexpr bool HAS_LOG = MODE != M_EAGER;
   static constexpr bool HAS_TOKEN = MODE == M_EAGER || MODE == M_STEP || MODE == M_MERGE;
   static constexpr bool READS_OUT = MODE != M_FLUSH;
@@ -293,12 +310,13 @@ struct Cfg {
   static_assert(CH == EPP, "the first merge chunk is staged by the first coefficient pass");
   static_assert(LPE <= 64 && 64 % LPE == 0, "an entry's lanes share one wave");
   static_assert(NT == threads_per_head(DK, DV), "launch bound must match the layout");
+  static_assert(!(BONUS && DL == 1), "the bonus readout is only defined with per-key decay");
 };
 
+// U_log holds the delta rule's corrected values in fp32, and exact copies of v (in the
+// activation dtype) for every other operator.
 template <int OP, typename TIN>
-struct UType { using type = float; };          // GDN/KDA: U_log holds corrected values, fp32
-template <typename TIN>
-struct UType<OP_RWKV6, TIN> { using type = TIN; };  // RWKV6: U_log holds exact copies of v
+struct UType { using type = std::conditional_t<OpTraits<OP>::DELTA, float, TIN>; };
 
 #if DL_WAVES_PER_EU > 0
 #define DL_OCCUPANCY __attribute__((amdgpu_waves_per_eu(DL_WAVES_PER_EU)))
@@ -388,11 +406,11 @@ void deltalog_kernel(KParams p) {
   float lam = 0.f, ell = 0.f, uf = 0.f;
   if constexpr (CF::HAS_TOKEN) {
     k_raw = kin[rl];
-    lam = p.lam[th * DL + rd];
-    if constexpr (!CF::DELTA) uf = p.u[size_t(h) * DK + rl];
+    if constexpr (CF::DECAY) lam = p.lam[th * DL + rd];
+    if constexpr (CF::BONUS) uf = p.u[size_t(h) * DK + rl];
   }
   if constexpr (CF::READS_OUT) q_raw = qin[rl];
-  if constexpr (CF::HAS_LOG) ell = p.ell[sh * DL + rd];
+  if constexpr (CF::HAS_LOG && CF::DECAY) ell = p.ell[sh * DL + rd];
   Raw4<TIN> v_raw{};
   float beta = 0.f;
   if constexpr (CF::HAS_TOKEN) {
@@ -428,7 +446,7 @@ void deltalog_kernel(KParams p) {
   }
 
   const TIN* Kb = static_cast<const TIN*>(p.k_log) + sh * size_t(C) * DK;
-  const float* Lb = p.lam_log + sh * size_t(C) * DL;
+  const float* Lb = CF::DECAY ? p.lam_log + sh * size_t(C) * DL : nullptr;
   const TU* Ub = static_cast<const TU*>(p.u_log) + sh * size_t(C) * DV;
   const int e_ = tid / CF::LPE;                   // coefficient pass: entry within the pass
   const int c_ = tid % CF::LPE;                   //                   key-row run
@@ -449,8 +467,11 @@ void deltalog_kernel(KParams p) {
   if constexpr (CF::REPLAYS && DL_PREFETCH_KEYS && (DL == 1 || kPrefetchPerKey)) {
     const int ek = min(e_, Lm1);
     kr_raw.load(Kp + size_t(ek) * DK + c_ * RPL);
-    if constexpr (DL == 1) lr0 = Lp[ek];
-    else lr_raw.load(Lp + size_t(ek) * DK + c_ * RPL);
+    if constexpr (DL == 1) {
+      if constexpr (CF::DECAY) lr0 = Lp[ek];
+    } else {
+      lr_raw.load(Lp + size_t(ek) * DK + c_ * RPL);
+    }
   }
   Raw4<TU> up0_raw{}, up1_raw{};                     // first two replay values of this row group
   if constexpr (CF::REPLAYS && DL_PREFETCH_U) {
@@ -479,12 +500,14 @@ void deltalog_kernel(KParams p) {
   // ---- 4. per-row decay factors (LDS) and the token dot product ---------------------
   if (r0 < DK) {
     float lr, lm;
+    // Readouts of the decayed state (the delta-rule correction, and the post-update
+    // output's base part), except RWKV6, which reads the old state.
     if constexpr (MODE == M_EAGER) {
-      lr = CF::DELTA ? lam : 0.f;   // delta rule reads the decayed state; RWKV6 the old one
+      lr = CF::BONUS ? 0.f : lam;
       lm = lam;
     } else if constexpr (MODE == M_STEP || MODE == M_MERGE) {
       lm = ell + lam;
-      lr = CF::DELTA ? lm : ell;
+      lr = CF::BONUS ? ell : lm;
     } else {                        // FLUSH, READOUT: the represented state as it stands
       lr = ell;
       lm = ell;
@@ -501,8 +524,8 @@ void deltalog_kernel(KParams p) {
     }
   }
   if constexpr (CF::HAS_TOKEN) {
-    // q.k (delta rule, post-update readout) or r.(u*k) (RWKV6 bonus)
-    float d = CF::DELTA ? qf * kf : qf * uf * kf;
+    // q.k (post-update readout of the new term) or r.(u*k) (RWKV6 bonus)
+    float d = CF::BONUS ? qf * uf * kf : qf * kf;
     if (r0 >= DK) d = 0.f;                        // threads past dk hold a repeated row
 #pragma unroll
     for (int m = 32; m >= 1; m >>= 1) d += shfl_xor(d, m);
@@ -512,8 +535,8 @@ void deltalog_kernel(KParams p) {
 
   // ---- 5. replay coefficients g_i(k), g_i(q) of the live entries --------------------
   // A merging workgroup also writes the first chunk of decayed keys
-  // K~_i[r] = e^(l'_r - Lam_i,r) K_i[r] to LDS here, from the same loads (for the delta
-  // rule the merge decay l' equals the readout decay; RWKV6 reads at ell, merges at l').
+  // K~_i[r] = e^(l'_r - Lam_i,r) K_i[r] to LDS here, from the same loads (the merge
+  // decay l' equals the readout decay, except for RWKV6, which reads at ell).
   if constexpr (CF::REPLAYS) {
     for (int i0 = 0; i0 < L; i0 += CF::EPP) {     // uniform trip count
       const int i = i0 + e_;
@@ -522,8 +545,11 @@ void deltalog_kernel(KParams p) {
       if (i < L) {
         if (i0 > 0 || !DL_PREFETCH_KEYS || (DL != 1 && !kPrefetchPerKey)) {
           ld_run<RPL>(Kb + size_t(i) * DK + c_ * RPL, kr);
-          if constexpr (DL == 1) lr_[0] = Lb[i];
-          else ld_run<RPL>(Lb + size_t(i) * DK + c_ * RPL, lr_);
+          if constexpr (DL == 1) {
+            if constexpr (CF::DECAY) lr_[0] = Lb[i];
+          } else {
+            ld_run<RPL>(Lb + size_t(i) * DK + c_ * RPL, lr_);
+          }
         } else {
           kr_raw.get(kr);
           if constexpr (DL == 1) lr_[0] = lr0;
@@ -536,7 +562,7 @@ void deltalog_kernel(KParams p) {
             ak = fmaf(kr[x], s_kf[r], ak);
             aq = fmaf(kr[x], s_qf[r], aq);
           }
-          const float w = dl_exp(s_lr[0] - lr_[0]);
+          const float w = CF::DECAY ? dl_exp(s_lr[0] - lr_[0]) : 1.f;
           ak *= w;
           aq *= w;
           if (stage) {
@@ -550,7 +576,7 @@ void deltalog_kernel(KParams p) {
             const float wk = dl_exp(s_lr[r] - lr_[x]) * kr[x];
             ak = fmaf(wk, s_kf[r], ak);
             aq = fmaf(wk, s_qf[r], aq);
-            if (stage) s_kt[r * CF::KTS + e_] = CF::DELTA ? wk : dl_exp(s_lm[r] - lr_[x]) * kr[x];
+            if (stage) s_kt[r * CF::KTS + e_] = CF::BONUS ? dl_exp(s_lm[r] - lr_[x]) * kr[x] : wk;
           }
         }
       } else if (stage) {
@@ -640,8 +666,8 @@ void deltalog_kernel(KParams p) {
       bv = beta * (vv - cv);                // b = beta (v - c)
       ov = fma4(dot, bv, ov);               // + (q.k) b : post-update readout
     } else {
-      bv = vv;                              // RWKV6: b = v
-      ov = fma4(dot, vv, ov);               // + (r.(u*k)) v : bonus
+      bv = vv;                              // b = v
+      ov = fma4(dot, vv, ov);               // + (q.k) v, or the RWKV6 bonus (r.(u*k)) v
     }
   }
   if constexpr (CF::READS_OUT) {
@@ -662,9 +688,11 @@ void deltalog_kernel(KParams p) {
       constexpr int KCH = DK * int(sizeof(TIN)) / 16;   // 16-byte chunks of one key row
       for (int x = tid; x < KCH; x += NT)
         reinterpret_cast<uint4*>(Kd)[x] = reinterpret_cast<const uint4*>(kin)[x];
-      for (int x = tid; x < DL; x += NT) {
-        p.lam_log[ent * DL + x] = s_lm[x];
-        p.ell[sh * DL + x] = s_lm[x];
+      if constexpr (CF::DECAY) {
+        for (int x = tid; x < DL; x += NT) {
+          p.lam_log[ent * DL + x] = s_lm[x];
+          p.ell[sh * DL + x] = s_lm[x];
+        }
       }
       if (tid == 0) p.len[sh] = L + 1;
       return;
@@ -691,8 +719,11 @@ void deltalog_kernel(KParams p) {
           float val = 0.f;
           if (ii < n) {
             const int i = i0 + ii;
-            const float lam_i = Lb[size_t(i) * DL + ((DL == 1) ? 0 : r)];
-            val = dl_exp(s_lm[(DL == 1) ? 0 : r] - lam_i) * ld1(Kb + size_t(i) * DK + r);
+            val = ld1(Kb + size_t(i) * DK + r);
+            if constexpr (CF::DECAY) {
+              const float lam_i = Lb[size_t(i) * DL + ((DL == 1) ? 0 : r)];
+              val *= dl_exp(s_lm[(DL == 1) ? 0 : r] - lam_i);
+            }
           }
           s_kt[r * CF::KTS + ii] = val;             // K~_i[r] = e^(l'_r - Lam_i,r) K_i[r]
         }
@@ -722,7 +753,8 @@ void deltalog_kernel(KParams p) {
 #pragma unroll
     for (int j = 0; j < RPT; ++j) StateQuad<TS>::store(srs, toff, j * kRowBlock, m[j]);
     if constexpr (CF::HAS_LOG) {
-      for (int x = tid; x < DL; x += NT) p.ell[sh * DL + x] = 0.f;
+      if constexpr (CF::DECAY)
+        for (int x = tid; x < DL; x += NT) p.ell[sh * DL + x] = 0.f;
       if (tid == 0) p.len[sh] = 0;
     }
   }

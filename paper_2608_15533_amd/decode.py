@@ -43,8 +43,8 @@ list a graph reads is a fixed device buffer that the engine refreshes with one s
 host-to-device copy, outside the graph, when the plan's row order changes.
 
 Slot lifecycle (Sec. 4): ``admit`` writes the prefill state into the slot's dense base
-and resets only the slot's auxiliary buffers (cumulative log-decay and live length; log
-rows past the live length are never read).  ``release`` frees the slot, optionally
+and resets only the slot's auxiliary buffers (cumulative log-decay, where the operator
+has one, and live length; log rows past the live length are never read).  ``release`` frees the slot, optionally
 flushing its log into the base first so the materialised state can be saved.
 """
 
@@ -65,8 +65,10 @@ class LayerInputs:
         self.q = torch.zeros((n, H, dk), dtype=it, device=device)
         self.k = torch.zeros((n, H, dk), dtype=it, device=device)
         self.v = torch.zeros((n, H, dv), dtype=it, device=device)
-        self.lam = torch.zeros((n, H) if desc.op == D.DL_OP_GDN else (n, H, dk), **f32)
-        self.beta = None if desc.op == D.DL_OP_RWKV6 else torch.zeros((n, H), **f32)
+        dl = D.decay_width(desc)
+        self.lam = (None if dl == 0 else
+                    torch.zeros((n, H) if dl == 1 else (n, H, dl), **f32))
+        self.beta = torch.zeros((n, H), **f32) if desc.op in D.DELTA_OP_IDS else None
         self.u = torch.zeros((H, dk), **f32) if desc.op == D.DL_OP_RWKV6 else None
         self._tokens = {}
 
@@ -76,8 +78,8 @@ class LayerInputs:
         tok = self._tokens.get((r0, r1))
         if tok is None:
             tok = D.Token(self.desc, r1 - r0, self.q[r0:r1], self.k[r0:r1], self.v[r0:r1],
-                          self.lam[r0:r1], None if self.beta is None else self.beta[r0:r1],
-                          self.u)
+                          None if self.lam is None else self.lam[r0:r1],
+                          None if self.beta is None else self.beta[r0:r1], self.u)
             self._tokens[(r0, r1)] = tok
         return tok
 
@@ -87,7 +89,8 @@ class LayerInputs:
         self.q[idx] = q.to(self.q.device, self.q.dtype)
         self.k[idx] = k.to(self.k.device, self.k.dtype)
         self.v[idx] = v.to(self.v.device, self.v.dtype)
-        self.lam[idx] = lam.to(self.lam.device, torch.float32)
+        if self.lam is not None:
+            self.lam[idx] = lam.to(self.lam.device, torch.float32)
         if self.beta is not None:
             self.beta[idx] = beta.to(self.beta.device, torch.float32)
 
@@ -134,7 +137,8 @@ class DecodeEngine:
                 st.S[slot].zero_()
             else:
                 st.S[slot].copy_(prefill[layer])
-            st.ell[slot].zero_()
+            if st.ell is not None:
+                st.ell[slot].zero_()
             st.len[slot].zero_()
         self.plan = None
         return slot

@@ -31,9 +31,12 @@ DL_ABI_VERSION = 2
 DL_MAX_MERGE_INTERVAL = 64
 DL_OK, DL_E_NULL, DL_E_SHAPE, DL_E_DTYPE, DL_E_ALIGN, DL_E_UNSUPPORTED, DL_E_HIP, DL_E_VERSION = (
     0, -1, -2, -3, -4, -5, -6, -7)
-DL_OP_GDN, DL_OP_KDA, DL_OP_RWKV6 = 0, 1, 2
+DL_OP_GDN, DL_OP_KDA, DL_OP_RWKV6, DL_OP_LINATTN, DL_OP_RETNET, DL_OP_GLA = 0, 1, 2, 3, 4, 5
 DL_F32, DL_BF16 = 0, 1
-OP_IDS = {"gdn": DL_OP_GDN, "kda": DL_OP_KDA, "rwkv6": DL_OP_RWKV6}
+OP_IDS = {"gdn": DL_OP_GDN, "kda": DL_OP_KDA, "rwkv6": DL_OP_RWKV6, "linattn": DL_OP_LINATTN,
+          "retnet": DL_OP_RETNET, "gla": DL_OP_GLA}
+DELTA_OP_IDS = (DL_OP_GDN, DL_OP_KDA)                  # b = beta (v - correction); needs beta
+PER_KEY_OP_IDS = (DL_OP_KDA, DL_OP_RWKV6, DL_OP_GLA)   # lambda is [.., dk]; else one per head
 DTYPE_IDS = {"f32": DL_F32, "bf16": DL_BF16}
 TORCH_DTYPES = {"f32": torch.float32, "bf16": torch.bfloat16}
 
@@ -97,14 +100,22 @@ if dl_abi_version() != DL_ABI_VERSION:
 
 # ----------------------------------------------------------------- descriptors
 def make_desc(op, B, H, dk, dv, M, in_dtype="bf16", state_dtype="f32"):
-    """dl_desc for operator ``op`` ("gdn"/"kda"/"rwkv6") with merge interval M."""
-    u_dtype = in_dtype if op == "rwkv6" else "f32"
+    """dl_desc for operator ``op`` (a key of ``OP_IDS``) with merge interval M."""
+    u_dtype = "f32" if OP_IDS[op] in DELTA_OP_IDS else in_dtype
     return dl_desc(DL_ABI_VERSION, OP_IDS[op], B, H, dk, dv, M, DTYPE_IDS[in_dtype],
                    DTYPE_IDS[u_dtype], DTYPE_IDS[state_dtype])
 
 
 def state_torch_dtype(desc):
     return torch.bfloat16 if desc.state_dtype == DL_BF16 else torch.float32
+
+
+def decay_width(desc):
+    """Width of lambda, ell and the Lam_log snapshots: dk (per-key decay) or 1 (one value
+    per head); 0 for linear attention, which has no decay."""
+    if desc.op == DL_OP_LINATTN:
+        return 0
+    return desc.dk if desc.op in PER_KEY_OP_IDS else 1
 
 
 def _ptr(t):
@@ -130,30 +141,31 @@ class DeltaLogState:
     S [B,H,dk,dv] state dtype, ell [B,H,dl] f32, k_log [B,H,C,dk] in_dtype,
     u_log [B,H,C,dv], lam_log [B,H,C,dl] f32, len [B,H] int32, err [1] int32.  ``S``
     starts as a copy of ``S0`` (the prefill state, converted to the state dtype); the
-    log starts empty (Sec. 4 slot lifecycle).
+    log starts empty (Sec. 4 slot lifecycle).  Linear attention has no decay: ``ell``
+    and ``lam_log`` are None and passed to the library as NULL.
     """
 
     def __init__(self, desc, S0=None, device="cuda"):
         self.desc = desc
         B, H, dk, dv, M = desc.num_slots, desc.heads, desc.dk, desc.dv, desc.merge_interval
         C = M - 1
-        dl = 1 if desc.op == DL_OP_GDN else dk
+        dl = decay_width(desc)
         in_t = torch.bfloat16 if desc.in_dtype == DL_BF16 else torch.float32
         u_t = torch.bfloat16 if desc.u_log_dtype == DL_BF16 else torch.float32
         f32 = dict(dtype=torch.float32, device=device)
         st = state_torch_dtype(desc)
         self.S = (torch.zeros((B, H, dk, dv), dtype=st, device=device) if S0 is None else
                   S0.to(device=device, dtype=st).contiguous().clone())
-        self.ell = torch.zeros((B, H, dl), **f32)
+        self.ell = torch.zeros((B, H, dl), **f32) if dl else None
         self.k_log = torch.zeros((B, H, max(C, 0), dk), dtype=in_t, device=device)
         self.u_log = torch.zeros((B, H, max(C, 0), dv), dtype=u_t, device=device)
-        self.lam_log = torch.zeros((B, H, max(C, 0), dl), **f32)
+        self.lam_log = torch.zeros((B, H, max(C, 0), dl), **f32) if dl else None
         self.len = torch.zeros((B, H), dtype=torch.int32, device=device)
         self.err = torch.zeros((1,), dtype=torch.int32, device=device)
         self.struct = dl_state(_ptr(self.S), _ptr(self.ell),
                                _ptr(self.k_log) if C > 0 else None,
                                _ptr(self.u_log) if C > 0 else None,
-                               _ptr(self.lam_log) if C > 0 else None,
+                               _ptr(self.lam_log) if C > 0 and dl else None,
                                _ptr(self.len), _ptr(self.err))
 
     def buffers(self):
@@ -166,16 +178,23 @@ class Token:
 
     def __init__(self, desc, n, q, k, v, lam, beta=None, u=None):
         H, dk, dv = desc.heads, desc.dk, desc.dv
-        dl = 1 if desc.op == DL_OP_GDN else dk
+        dl = decay_width(desc)
         it = torch.bfloat16 if desc.in_dtype == DL_BF16 else torch.float32
         _need(q, "q", it, (n, H, dk))
         _need(k, "k", it, (n, H, dk))
         _need(v, "v", it, (n, H, dv))
-        _need(lam, "lam", torch.float32, (n, H) if dl == 1 else (n, H, dl))
+        if dl:
+            _need(lam, "lam", torch.float32, (n, H) if dl == 1 else (n, H, dl))
+        else:
+            lam = None                       # linear attention: no decay input
         if desc.op == DL_OP_RWKV6:
             _need(u, "u", torch.float32, (H, dk))
         else:
+            u = None
+        if desc.op in DELTA_OP_IDS:
             _need(beta, "beta", torch.float32, (n, H))
+        else:
+            beta = None
         self.n = n
         self.tensors = (q, k, v, lam, beta, u)
         self.struct = dl_token(_ptr(q), _ptr(k), _ptr(v), _ptr(beta), _ptr(lam), _ptr(u))

@@ -36,8 +36,9 @@ def token(desc, x, u=None, rows=None):
     n = x["q"].shape[0]
     beta = None if x.get("beta") is None else to_dev(x["beta"], torch.float32)
     ud = None if u is None else to_dev(u, torch.float32)
+    lam = None if x.get("lam") is None else to_dev(x["lam"], torch.float32)
     return dl.Token(desc, n, to_dev(x["q"], it), to_dev(x["k"], it), to_dev(x["v"], it),
-                    to_dev(x["lam"], torch.float32), beta, ud)
+                    lam, beta, ud)
 
 
 def sub(x, rows):

@@ -76,7 +76,8 @@ def test_null_descriptor():
 
 @pytest.mark.parametrize("field,value,code", [
     ("abi_version", 1, D.DL_E_VERSION),
-    ("op", 3, D.DL_E_UNSUPPORTED),
+    ("op", 6, D.DL_E_UNSUPPORTED),
+    ("op", -1, D.DL_E_UNSUPPORTED),
     ("dk", 96, D.DL_E_UNSUPPORTED),
     ("dv", 256, D.DL_E_UNSUPPORTED),
     ("merge_interval", 0, D.DL_E_UNSUPPORTED),
@@ -141,6 +142,33 @@ def test_token_nulls(field):
 def test_rwkv6_needs_bonus():
     d = D.make_desc("rwkv6", 4, 2, 64, 64, 16, "bf16")
     assert append(d, t=token(beta=None)) == D.DL_E_NULL
+
+
+def test_linear_attention_takes_no_decay_buffers():
+    """Linear attention has no decay: NULL lam, ell and lam_log (and beta) pass the checks
+    (the call then stops at the misaligned output)."""
+    d = D.make_desc("linattn", 4, 2, 128, 128, 16, "bf16")
+    s = state(ell=None, lam_log=None)
+    assert append(d, s=s, t=token(lam=None, beta=None), o=A + 4) == D.DL_E_ALIGN
+    assert append(d, s=state(k_log=None), t=token(lam=None, beta=None)) == D.DL_E_NULL
+
+
+@pytest.mark.parametrize("op", ["retnet", "gla"])
+def test_decaying_additive_operators_need_lam_not_beta(op):
+    d = D.make_desc(op, 4, 2, 128, 128, 16, "bf16")
+    assert append(d, t=token(beta=None), o=A + 4) == D.DL_E_ALIGN
+    assert append(d, t=token(lam=None, beta=None)) == D.DL_E_NULL
+    assert append(d, s=state(ell=None), t=token(beta=None)) == D.DL_E_NULL
+    assert append(d, s=state(lam_log=None), t=token(beta=None)) == D.DL_E_NULL
+
+
+@pytest.mark.parametrize("op", ["linattn", "retnet", "gla"])
+def test_additive_u_log_holds_copies_of_v(op):
+    """U_log of the operators without a correction holds v in the activation dtype."""
+    d = D.make_desc(op, 4, 2, 128, 128, 16, "bf16")
+    assert d.u_log_dtype == D.DL_BF16
+    d.u_log_dtype = D.DL_F32
+    assert append(d, t=token(beta=None)) == D.DL_E_DTYPE
 
 
 @pytest.mark.parametrize("where,field,off", [

@@ -34,7 +34,8 @@ TRACE = {
     10: [("admit", 5)],
     13: [("release", 3, True), ("admit", 6)],
 }
-SHAPES = {"gdn": (4, 128, 128), "kda": (4, 128, 128), "rwkv6": (4, 64, 64)}
+SHAPES = {"gdn": (4, 128, 128), "kda": (4, 128, 128), "rwkv6": (4, 64, 64),
+          "linattn": (4, 128, 128), "retnet": (4, 64, 64), "gla": (4, 128, 64)}
 
 
 def _request(op, r):
@@ -130,14 +131,14 @@ def run_trace(op, mode, graphs, oracle=False):
     return outs, saved, eng
 
 
-@pytest.mark.parametrize("op", ["gdn", "kda", "rwkv6"])
+@pytest.mark.parametrize("op", list(SHAPES))
 @pytest.mark.parametrize("mode", ["fused", "phased", "phased_concurrent"])
 def test_trace_against_oracle(op, mode):
     _, _, eng = run_trace(op, mode, graphs=True, oracle=True)
     assert eng.replays > 0
 
 
-@pytest.mark.parametrize("op", ["gdn", "rwkv6"])
+@pytest.mark.parametrize("op", ["gdn", "rwkv6", "linattn"])
 def test_modes_and_graphs_bitwise_equal(op):
     """Every scheduling mode, with and without graphs, gives bit-identical outputs and
     flushed states: the same kernel arithmetic on the same rows."""

@@ -37,6 +37,7 @@ def test_gdn_b1_h2_d64_m8(in_dtype, eager):
 MID = [
     ("gdn", W.GDN_B64, 16), ("kda", W.KDA_B128, 8), ("kda", W.KDA_B128, 16),
     ("kda", W.KDA_B128, 32), ("rwkv6", W.RWKV6_B128, 16),
+    ("linattn", W.LINATTN_B64, 16), ("retnet", W.RETNET_B64, 16), ("gla", W.GLA_B128, 16),
 ]
 
 
@@ -55,6 +56,9 @@ FULL = [
     ("kda_b128_h32_d128_m16", W.KDA_B128, 16, [2, 77, 126]),
     ("kda_b128_h32_d128_m32", W.KDA_B128, 32, [3, 90, 125]),
     ("rwkv6_b128_h40_d64_m16", W.RWKV6_B128, 16, [0, 55, 127]),
+    ("linattn_b64_h32_d128_m16", W.LINATTN_B64, 16, [0, 21, 63]),
+    ("retnet_b64_h32_d128_m16", W.RETNET_B64, 16, [5, 40, 62]),
+    ("gla_b128_h32_d128_m16", W.GLA_B128, 16, [4, 66, 127]),
 ]
 
 
@@ -79,7 +83,9 @@ def test_serving_stack_layer_staggered(layer):
     _check(r, f"stack layer {layer} staggered")
 
 
-BF16_STATE = [("gdn", W.GDN_B64, 16), ("kda", W.KDA_B128, 16), ("rwkv6", W.RWKV6_B128, 16)]
+BF16_STATE = [("gdn", W.GDN_B64, 16), ("kda", W.KDA_B128, 16), ("rwkv6", W.RWKV6_B128, 16),
+              ("linattn", W.LINATTN_B64, 16), ("retnet", W.RETNET_B64, 16),
+              ("gla", W.GLA_B128, 16)]
 
 
 @pytest.mark.parametrize("op,w,M", BF16_STATE, ids=[o for o, _, _ in BF16_STATE])

@@ -15,13 +15,21 @@ from gpu_harness import TOL_F32_STATE, D, log, oracle_step, rel, to_dev, token
 
 pytestmark = pytest.mark.gpu
 
-OPS = ("gdn", "kda", "rwkv6")
+OPS = OE.OPS
 SHAPES = ((64, 64), (128, 128), (64, 128), (128, 64))
+WL = {"gdn": W.GDN_B64, "kda": W.KDA_B128, "rwkv6": W.RWKV6_B128,
+      "linattn": W.LINATTN_B64, "retnet": W.RETNET_B64, "gla": W.GLA_B128}
+
+
+def lam_rows(x, N):
+    """lambda of a step-input dict as [N, dl] rows (None for linear attention)."""
+    return None if x["lam"] is None else x["lam"].reshape(N, -1)
 
 
 def dyadic_inputs(op, B, H, dk, dv, steps, seed):
     """Inputs whose every intermediate is exact in fp32: one-hot keys, integer state and
-    values, queries with 4 entries in {-1, 1}, beta in {1, 1/2}, lambda = 0, dyadic u."""
+    values, queries with 4 entries in {-1, 1}, beta in {1, 1/2}, lambda = 0 (none for
+    linear attention), dyadic u."""
     rng = np.random.default_rng(seed)
     S0 = rng.integers(-3, 4, size=(B, H, dk, dv)).astype(np.float32)
     xs = []
@@ -35,8 +43,10 @@ def dyadic_inputs(op, B, H, dk, dv, steps, seed):
                 pos = rng.choice(dk, 4, replace=False)
                 q[b, h, pos] = rng.choice([-1.0, 1.0], 4)
         v = rng.integers(-4, 5, size=(B, H, dv)).astype(np.float32)
-        lam = np.zeros((B, H) if op == "gdn" else (B, H, dk), np.float32)
-        beta = None if op == "rwkv6" else rng.choice([1.0, 0.5], size=(B, H)).astype(np.float32)
+        lam = (None if op == "linattn" else
+               np.zeros((B, H) if op in ("gdn", "retnet") else (B, H, dk), np.float32))
+        beta = (rng.choice([1.0, 0.5], size=(B, H)).astype(np.float32)
+                if op in OE.DELTA_OPS else None)
         xs.append(dict(q=q, k=k, v=v, lam=lam, beta=beta))
     u = (rng.integers(-4, 5, size=(H, dk)) / 4.0).astype(np.float32) if op == "rwkv6" else None
     return S0, xs, u
@@ -108,7 +118,7 @@ def test_exact_dyadic_bitwise(op, dk, dv, in_dtype):
 def test_merge_interval_1_equals_eager_bitwise(op):
     """M = 1 makes every step a merge: the DeltaLog kernel must reproduce the eager
     kernel bit for bit (same arithmetic, same order)."""
-    w = {"gdn": W.GDN_B64, "kda": W.KDA_B128, "rwkv6": W.RWKV6_B128}[op].with_(B=4)
+    w = WL[op].with_(B=4)
     S0 = W.initial_state(w)
     xs = [W.step_inputs(w, t) for t in range(6)]
     u = W.bonus(w)
@@ -123,14 +133,14 @@ def test_merge_interval_1_equals_eager_bitwise(op):
 def _state_arrays(st):
     """Host copies of every state buffer (bf16 buffers widened to fp32, exactly)."""
     return {k: (v.float() if v.dtype == torch.bfloat16 else v).cpu().numpy().copy()
-            for k, v in st.buffers().items()}
+            for k, v in st.buffers().items() if v is not None}
 
 
 @pytest.mark.parametrize("op", OPS)
 def test_deterministic_and_slot_order_invariant(op):
     """Two runs are bitwise identical; running the slots in a permuted order (a shuffled
     slot list) gives every slot bitwise the same state, log and outputs."""
-    w = {"gdn": W.GDN_B64, "kda": W.KDA_B128, "rwkv6": W.RWKV6_B128}[op].with_(B=6)
+    w = WL[op].with_(B=6)
     M, steps = 4, 7
     S0 = W.initial_state(w)
     xs = [W.step_inputs(w, t) for t in range(steps)]
@@ -153,7 +163,7 @@ def test_deterministic_and_slot_order_invariant(op):
 def test_batch_composition_invariance(op):
     """A slot's result does not depend on which other slots share the launch: stepping
     slots in varying subsets equals stepping each subset's slots in full launches."""
-    w = {"gdn": W.GDN_B64, "kda": W.KDA_B128, "rwkv6": W.RWKV6_B128}[op].with_(B=5)
+    w = WL[op].with_(B=5)
     M, steps = 3, 6
     S0 = W.initial_state(w)
     xs = [W.step_inputs(w, t) for t in range(steps)]
@@ -172,7 +182,7 @@ def test_batch_composition_invariance(op):
         x = xs[t]
         o = model.step(x["q"].reshape(-1, w.dk), x["k"].reshape(-1, w.dk), x["v"].reshape(-1, w.dv),
                        None if x["beta"] is None else x["beta"].reshape(-1),
-                       x["lam"].reshape(w.B * w.H, -1), u=ub, active=act.reshape(-1))
+                       lam_rows(x, w.B * w.H), u=ub, active=act.reshape(-1))
         ref = o.reshape(w.B, w.H, w.dv)[rows]
         assert rel(o_part[t], ref) <= TOL_F32_STATE
     assert rel(st_part.S.cpu().numpy(), model.Sbar.reshape(w.B, w.H, w.dk, w.dv)) <= TOL_F32_STATE
@@ -182,9 +192,9 @@ def test_batch_composition_invariance(op):
 @pytest.mark.parametrize("op", OPS)
 def test_log_contents_match_the_model(op):
     """After L appends the log holds: K_log = k bitwise (exact copies), Lam_log and ell =
-    the cumulative log-decay, U_log = the delta-rule values b (GDN/KDA) or v bitwise
-    (RWKV6), len = L -- compared with the fp64 Alg. 1 model."""
-    w = {"gdn": W.GDN_B64, "kda": W.KDA_B128, "rwkv6": W.RWKV6_B128}[op].with_(B=3)
+    the cumulative log-decay (none for linear attention), U_log = the delta-rule values b
+    (GDN/KDA) or v bitwise (the others), len = L -- compared with the fp64 Alg. 1 model."""
+    w = WL[op].with_(B=3)
     M, steps = 8, 5
     S0 = W.initial_state(w)
     xs = [W.step_inputs(w, t) for t in range(steps)]
@@ -196,16 +206,19 @@ def test_log_contents_match_the_model(op):
     ub = None if u is None else np.broadcast_to(u, (w.B, w.H, w.dk)).reshape(N, w.dk)
     for x in xs:
         model.step(x["q"].reshape(N, -1), x["k"].reshape(N, -1), x["v"].reshape(N, -1),
-                   None if x["beta"] is None else x["beta"].reshape(N), x["lam"].reshape(N, -1), u=ub)
+                   None if x["beta"] is None else x["beta"].reshape(N), lam_rows(x, N), u=ub)
     a = _state_arrays(st)
     L = steps
     assert np.all(a["len"] == L)
     K = a["k_log"].astype(np.float64).reshape(N, M - 1, w.dk)[:, :L]
     np.testing.assert_array_equal(K, model.K[:, :L])
-    assert rel(a["lam_log"].reshape(N, M - 1, -1)[:, :L], model.Lam[:, :L]) <= 1e-6
-    assert rel(a["ell"].reshape(N, -1), model.ell) <= 1e-6
+    if op == "linattn":
+        assert "lam_log" not in a and "ell" not in a
+    else:
+        assert rel(a["lam_log"].reshape(N, M - 1, -1)[:, :L], model.Lam[:, :L]) <= 1e-6
+        assert rel(a["ell"].reshape(N, -1), model.ell) <= 1e-6
     U = a["u_log"].astype(np.float64).reshape(N, M - 1, w.dv)[:, :L]
-    if op == "rwkv6":
+    if op not in OE.DELTA_OPS:
         np.testing.assert_array_equal(U, model.U[:, :L])
     else:
         assert rel(U, model.U[:, :L]) <= TOL_F32_STATE
@@ -216,7 +229,7 @@ def test_log_contents_match_the_model(op):
 def test_readout_forced_merge_flush(op):
     """dl_readout equals q^T S_eager and mutates nothing; a forced merge at L < C equals
     the eager step; a flush materialises the eager state and empties the log."""
-    w = {"gdn": W.GDN_B64, "kda": W.KDA_B128, "rwkv6": W.RWKV6_B128}[op].with_(B=3)
+    w = WL[op].with_(B=3)
     dl = D()
     M = 16
     S0 = W.initial_state(w)
@@ -242,14 +255,16 @@ def test_readout_forced_merge_flush(op):
     torch.cuda.synchronize()
     assert rel(o.cpu().numpy(), ref_o[5]) <= TOL_F32_STATE
     assert rel(st.S.cpu().numpy(), ref_S[5]) <= TOL_F32_STATE
-    assert np.all(st.len.cpu().numpy() == 0) and np.all(st.ell.cpu().numpy() == 0)
+    assert np.all(st.len.cpu().numpy() == 0)
+    assert st.ell is None or np.all(st.ell.cpu().numpy() == 0)
     # three appends then a flush
     for t in (6, 7, 8):
         dl.dl_append_step(desc, st, token(desc, xs[t], u), o)
     dl.dl_merge(desc, st)
     torch.cuda.synchronize()
     assert rel(st.S.cpu().numpy(), ref_S[8]) <= TOL_F32_STATE
-    assert np.all(st.len.cpu().numpy() == 0) and np.all(st.ell.cpu().numpy() == 0)
+    assert np.all(st.len.cpu().numpy() == 0)
+    assert st.ell is None or np.all(st.ell.cpu().numpy() == 0)
     # a flush of an empty log changes nothing
     S_now = st.S.cpu().numpy().copy()
     dl.dl_merge(desc, st)
@@ -277,7 +292,7 @@ def test_rectangular_heads(op, dk, dv):
 @pytest.mark.parametrize("op", OPS)
 def test_largest_merge_interval(op):
     """M = 64 (63 live entries, merged in 4 staged chunks) over 70 steps."""
-    base = {"gdn": W.GDN_B64, "kda": W.KDA_B128, "rwkv6": W.RWKV6_B128}[op]
+    base = WL[op]
     w = base.with_(B=2, H=2, M=64, steps=70)
     S0 = W.initial_state(w)
     xs = [W.step_inputs(w, t) for t in range(w.steps)]
