@@ -215,7 +215,8 @@ def decode_loop(args):
                 for _ in range(min(per_step, eng.sched.free_slots)):
                     slot = eng.sched.admit()           # the base already holds a state
                     for st in eng.states:
-                        st.ell[slot].zero_()
+                        if st.ell is not None:
+                            st.ell[slot].zero_()
                         st.len[slot].zero_()
                 eng.schedule()
                 eng.step()
@@ -465,7 +466,8 @@ def main():
             "dv": w.dv, "merge_interval": w.M, "in_dtype": w.in_dtype, "state_dtype": sd,
             "layer_states": R, "state_MiB_per_layer": state_mib,
             "working_set_MiB": round(sum(t.numel() * t.element_size() for st in states
-                                         for t in st.buffers().values()) / 2**20, 1),
+                                         for t in st.buffers().values()
+                                         if t is not None) / 2**20, 1),
             "tokens_per_s_definition": ("per-layer token-updates/s = B*R*K/elapsed"
                                         if w.layers == 1 else
                                         "tokens through all layers = B*K/elapsed"),
