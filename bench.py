@@ -73,6 +73,12 @@ def parse():
                     help="override the workload's sequence count B (0: workload default)")
     ap.add_argument("--state-dtype", default="f32", choices=("f32", "bf16"),
                     help="dtype of the dense state (bf16: rounded on every store)")
+    ap.add_argument("--tiled", type=int, default=0, choices=(0, 2, 4), metavar="NV",
+                    help="time the value-tiled step (dl_append_step_tiled) with NV value tiles "
+                         "per head instead of the one-workgroup-per-head kernel")
+    ap.add_argument("--fused-replay", action="store_true",
+                    help="with --tiled: every tile recomputes the replay coefficients "
+                         "(default: split replay, prepared once per head)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--decode-loop", default="", metavar="MODES",
@@ -118,8 +124,11 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
-def profile_key(workload, state_dtype):
-    return workload + ("_bf16state" if state_dtype == "bf16" else "")
+def profile_key(workload, state_dtype, tiled=0, fused_replay=False):
+    key = workload + ("_bf16state" if state_dtype == "bf16" else "")
+    if tiled:
+        key += f"_tiled{tiled}" + ("_fused" if fused_replay else "_split")
+    return key
 
 
 def counter_traffic(key):
@@ -346,6 +355,16 @@ def main():
     eag = D.lib.dl_eager_step
     app_args = [[(dref, ctypes.byref(states[r].struct), ctypes.byref(toks[t].struct),
                   outs[r].data_ptr(), None, w.B, sp) for t in range(POOL)] for r in range(R)]
+    if args.tiled:
+        # value-tiled path: [ReplayPrep] + tiles + Finalize per layer and step; one
+        # scratch buffer serves every layer (the launches are ordered on one stream)
+        split = not args.fused_replay
+        ws = D.tiled_workspace(desc, w.B) if split else None
+        wsp, wsn = (None, 0) if ws is None else (ws.data_ptr(), ws.numel())
+        app = D.lib.dl_append_step_tiled
+        app_args = [[(dref, ctypes.byref(states[r].struct), ctypes.byref(toks[t].struct),
+                      outs[r].data_ptr(), None, w.B, args.tiled, int(split), wsp, wsn, sp)
+                     for t in range(POOL)] for r in range(R)]
     eag_args = [[(dref, eager_S[r].data_ptr(), ctypes.byref(toks[t].struct),
                   outs[r].data_ptr(), None, w.B, sp) for t in range(POOL)] for r in range(R)]
 
@@ -437,7 +456,8 @@ def main():
     eg_us = eg_ms * 1e3 / n_launch
     eg_gbs = eg_bytes / (eg_us * 1e-6) / 1e9
 
-    traffic, traffic_src = counter_traffic(profile_key(args.workload, sd))
+    traffic, traffic_src = counter_traffic(profile_key(args.workload, sd, args.tiled,
+                                                       args.fused_replay))
     state_mib = heads * w.dk * w.dv * (2 if sd == "bf16" else 4) / 2**20
     kname = {"gdn": "GDN", "kda": "KDA", "rwkv6": "RWKV6", "linattn": "LinearAttention",
              "retnet": "RetNet", "gla": "GLA"}[w.op]
@@ -461,7 +481,9 @@ def main():
                          f"M={w.M}" + (f", {w.layers} layers, staggered log fill"
                                        if w.layers > 1 else "")),
             "name": args.workload + (f" M={w.M}" if args.merge_interval else "")
-                    + (f" B={w.B}" if args.batch else ""),
+                    + (f" B={w.B}" if args.batch else "")
+                    + (f" tiled{args.tiled}-{'fused' if args.fused_replay else 'split'}"
+                       if args.tiled else ""),
             "op": w.op, "batch": w.B, "heads": w.H, "dk": w.dk,
             "dv": w.dv, "merge_interval": w.M, "in_dtype": w.in_dtype, "state_dtype": sd,
             "layer_states": R, "state_MiB_per_layer": state_mib,
@@ -474,8 +496,12 @@ def main():
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": f"deltalog_kernel<{kname},{w.dk},{w.dv},STEP,{w.in_dtype},{sd} state> "
-                      "(dl_append_step: append or merge)",
+            "kernel": (f"deltalog_kernel<{kname},{w.dk},{w.dv},STEP,{w.in_dtype},{sd} state> "
+                       "(dl_append_step: append or merge)" if not args.tiled else
+                       f"dl_append_step_tiled, {args.tiled} value tiles, "
+                       f"{'fused' if args.fused_replay else 'split'} replay: "
+                       "[replay_prep_kernel] + tile_step_kernel + finalize_kernel per call "
+                       "(durations and bytes are per call)"),
             "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",

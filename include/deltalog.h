@@ -45,6 +45,7 @@
 #ifndef DELTALOG_H
 #define DELTALOG_H
 
+#include <stddef.h>
 #include <stdint.h>
 #include <hip/hip_runtime_api.h>
 
@@ -154,6 +155,33 @@ int dl_merge(const dl_desc* desc, const dl_state* state, const dl_token* tok, fl
  * x [n,H,dk] in in_dtype.  Mutates nothing.  (No RWKV6 bonus: there is no token.) */
 int dl_readout(const dl_desc* desc, const dl_state* state, const void* q, float* o,
                const int32_t* slots, int32_t n, hipStream_t stream);
+
+/* Value-tiled DeltaLog step (Sec. 3.3, the kernel ownership path): the same operation
+ * as dl_append_step (results equal up to floating-point reassociation), with each
+ * (slot, head) state split along the value dimension into value_tiles tiles of
+ * dk x dv/value_tiles, one workgroup each.  Three launches on the stream:
+ *   [ReplayPrep]  split_replay != 0 and C > 0 only: the key-side replay coefficients
+ *                 q^T D(ell - Lam_i) K_i and k^T D(ell - Lam_i) K_i of every live entry,
+ *                 once per (row, head), into the caller's workspace (fp32);
+ *   AppendDecode  per value tile: stream the tile, replay the log on its columns (with
+ *                 the prepared coefficients, or recomputing them per tile when
+ *                 split_replay == 0), write the output slice, append the tile's U_log
+ *                 shard (tile 0 also writes K_log[L] and Lam_log[L]) or merge the tile;
+ *   Finalize      per (row, head): commit ell and L exactly once.
+ * value_tiles: 2 or 4.  Only state_dtype == DL_F32 (else DL_E_DTYPE).
+ * workspace: device memory of at least dl_tiled_workspace_bytes(desc, n) bytes, 16-byte
+ * aligned, owned by the caller; required when split_replay != 0 and C > 0, ignored
+ * otherwise.  Its contents are scratch: overwritten, never read across calls.  Calls
+ * that share a workspace must not overlap.  If a later launch fails, DL_E_HIP is
+ * returned and the earlier launches of the call may already be enqueued. */
+int dl_append_step_tiled(const dl_desc* desc, const dl_state* state, const dl_token* tok,
+                         float* o, const int32_t* slots, int32_t n, int32_t value_tiles,
+                         int32_t split_replay, void* workspace, size_t workspace_bytes,
+                         hipStream_t stream);
+
+/* Bytes of workspace dl_append_step_tiled needs for n rows with split replay:
+ * n * H * 2 * (M - 1) * sizeof(float) (0 when M == 1).  Writes *bytes. */
+int dl_tiled_workspace_bytes(const dl_desc* desc, int32_t n, size_t* bytes);
 
 /* Human-readable name of a dl_status value (static storage). */
 const char* dl_status_str(int status);

@@ -54,4 +54,16 @@ hipError_t launch_retnet(int mode, int dk, int dv, bool bf16, bool state_bf16, c
 hipError_t launch_gla(int mode, int dk, int dv, bool bf16, bool state_bf16, const KParams& p,
                       hipStream_t s);
 
+// Value-tiled step (fp32 state): [ReplayPrep into coef when split] -> tiles -> Finalize.
+#define DL_DECLARE_TILED(name)                                                          \
+  hipError_t launch_tiled_##name(int dk, int dv, bool bf16, int nv, bool split,          \
+                                 const KParams& p, float* coef, hipStream_t s)
+DL_DECLARE_TILED(gdn);
+DL_DECLARE_TILED(kda);
+DL_DECLARE_TILED(rwkv6);
+DL_DECLARE_TILED(linattn);
+DL_DECLARE_TILED(retnet);
+DL_DECLARE_TILED(gla);
+#undef DL_DECLARE_TILED
+
 }  // namespace dl

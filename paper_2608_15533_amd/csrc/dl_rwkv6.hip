@@ -1,9 +1,14 @@
 // RWKV6 instantiations of the DeltaLog decode kernels.
 #include "dl_launch.hpp"
+#include "dl_tiled.hpp"
 
 namespace dl {
 hipError_t launch_rwkv6(int mode, int dk, int dv, bool bf16, bool state_bf16, const KParams& p,
                         hipStream_t s) {
   return launch_op<OP_RWKV6>(mode, dk, dv, bf16, state_bf16, p, s);
+}
+hipError_t launch_tiled_rwkv6(int dk, int dv, bool bf16, int nv, bool split, const KParams& p,
+                              float* coef, hipStream_t s) {
+  return launch_tiled_op<OP_RWKV6>(dk, dv, bf16, nv, split, p, coef, s);
 }
 }  // namespace dl

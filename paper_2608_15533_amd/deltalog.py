@@ -40,7 +40,8 @@ PER_KEY_OP_IDS = (DL_OP_KDA, DL_OP_RWKV6, DL_OP_GLA)   # lambda is [.., dk]; els
 DTYPE_IDS = {"f32": DL_F32, "bf16": DL_BF16}
 TORCH_DTYPES = {"f32": torch.float32, "bf16": torch.bfloat16}
 
-EXPORTED = ("dl_eager_step", "dl_append_step", "dl_merge", "dl_readout", "dl_status_str",
+EXPORTED = ("dl_eager_step", "dl_append_step", "dl_merge", "dl_readout",
+            "dl_append_step_tiled", "dl_tiled_workspace_bytes", "dl_status_str",
             "dl_abi_version")
 
 
@@ -72,7 +73,13 @@ _lib.dl_merge.argtypes = [ctypes.POINTER(dl_desc), ctypes.POINTER(dl_state),
                           ctypes.POINTER(dl_token), _P, _P, ctypes.c_int32, _P]
 _lib.dl_readout.argtypes = [ctypes.POINTER(dl_desc), ctypes.POINTER(dl_state), _P, _P, _P,
                             ctypes.c_int32, _P]
-for _f in ("dl_eager_step", "dl_append_step", "dl_merge", "dl_readout", "dl_abi_version"):
+_lib.dl_append_step_tiled.argtypes = [ctypes.POINTER(dl_desc), ctypes.POINTER(dl_state),
+                                      ctypes.POINTER(dl_token), _P, _P, ctypes.c_int32,
+                                      ctypes.c_int32, ctypes.c_int32, _P, ctypes.c_size_t, _P]
+_lib.dl_tiled_workspace_bytes.argtypes = [ctypes.POINTER(dl_desc), ctypes.c_int32,
+                                          ctypes.POINTER(ctypes.c_size_t)]
+for _f in ("dl_eager_step", "dl_append_step", "dl_merge", "dl_readout", "dl_append_step_tiled",
+           "dl_tiled_workspace_bytes", "dl_abi_version"):
     getattr(_lib, _f).restype = ctypes.c_int
 _lib.dl_status_str.argtypes = [ctypes.c_int]
 _lib.dl_status_str.restype = ctypes.c_char_p
@@ -257,3 +264,32 @@ def dl_readout(desc, state, q, o, slots=None, stream=None):
     _need(o, "o", torch.float32, (n, desc.heads, desc.dv))
     _check(_lib.dl_readout(ctypes.byref(desc), ctypes.byref(state.struct), _ptr(q), _ptr(o),
                            sp, n, _stream(stream)), "dl_readout")
+
+
+def dl_tiled_workspace_bytes(desc, n):
+    """Bytes of scratch dl_append_step_tiled needs for n rows with split replay."""
+    out = ctypes.c_size_t(0)
+    _check(_lib.dl_tiled_workspace_bytes(ctypes.byref(desc), int(n), ctypes.byref(out)),
+           "dl_tiled_workspace_bytes")
+    return out.value
+
+
+def tiled_workspace(desc, n, device="cuda"):
+    """A device buffer of the split-replay scratch size for n rows (None if no log)."""
+    nbytes = dl_tiled_workspace_bytes(desc, n)
+    return torch.empty((nbytes,), dtype=torch.uint8, device=device) if nbytes else None
+
+
+def dl_append_step_tiled(desc, state, tok, o, slots=None, value_tiles=4, split_replay=True,
+                         workspace=None, stream=None):
+    """Value-tiled DeltaLog step (Sec. 3.3): the same operation as dl_append_step with
+    ``value_tiles`` workgroups per head; ``split_replay`` prepares the replay
+    coefficients once per head into ``workspace`` (see ``tiled_workspace``)."""
+    sp, n = _rows(desc, slots, tok.n)
+    _need(o, "o", torch.float32, (n, desc.heads, desc.dv))
+    wp, wn = (None, 0) if workspace is None else (workspace.data_ptr(), workspace.numel() *
+                                                  workspace.element_size())
+    _check(_lib.dl_append_step_tiled(ctypes.byref(desc), ctypes.byref(state.struct),
+                                     ctypes.byref(tok.struct), _ptr(o), sp, n,
+                                     int(value_tiles), int(bool(split_replay)), wp, wn,
+                                     _stream(stream)), "dl_append_step_tiled")

@@ -66,13 +66,14 @@ class Rollout:
     """
 
     def __init__(self, w, M=None, layer=0, sample=None, eager=False, B=None, steps=None,
-                 state_dtype="f32"):
+                 state_dtype="f32", tiled=None):
         self.dl = D()
         self.w = w if B is None else w.with_(B=B)
         self.M = w.M if M is None else M
         self.layer = layer
         self.steps = w.steps if steps is None else steps
         self.eager = eager
+        self.tiled = tiled                    # None, or (value_tiles, split_replay)
         w = self.w
         self.sample = np.arange(w.B) if sample is None else np.asarray(sample)
         self.desc = self.dl.make_desc(w.op, w.B, w.H, w.dk, w.dv, self.M, w.in_dtype,
@@ -88,6 +89,8 @@ class Rollout:
             self.state = self.dl.DeltaLogState(self.desc, to_dev(S0, torch.float32))
         self.S_ref = S0[self.sample].astype(np.float64)
         self.o = torch.empty((w.B, w.H, w.dv), dtype=torch.float32, device="cuda")
+        self.ws = (self.dl.tiled_workspace(self.desc, w.B)
+                   if tiled is not None and tiled[1] else None)
         self.err_out = 0.0
         self.err_state = 0.0
         self.n_state_checks = 0
@@ -105,6 +108,10 @@ class Rollout:
         o = self.o[:n]
         if self.eager:
             dl.dl_eager_step(self.desc, self.S, tok, o, slots=slots)
+        elif self.tiled is not None:
+            dl.dl_append_step_tiled(self.desc, self.state, tok, o, slots=slots,
+                                    value_tiles=self.tiled[0], split_replay=self.tiled[1],
+                                    workspace=self.ws)
         else:
             dl.dl_append_step(self.desc, self.state, tok, o, slots=slots)
         # oracle on the sampled slots that took this step

@@ -210,3 +210,37 @@ def test_other_entry_points_validate():
     assert D.lib.dl_merge(ctypes.byref(d), None, None, None, None, 4, None) == D.DL_E_NULL
     assert D.lib.dl_readout(ctypes.byref(d), ctypes.byref(state()), None, A, None, 4, None) == D.DL_E_NULL
     assert D.lib.dl_readout(ctypes.byref(d), ctypes.byref(state()), A + 8, A, None, 4, None) == D.DL_E_ALIGN
+
+
+def tiled(d, s=None, t=None, o=A + 0xB00000, slots=None, n=4, nv=4, split=1, ws=A + 0xD00000,
+          wsb=1 << 20):
+    return D.lib.dl_append_step_tiled(ctypes.byref(d), ctypes.byref(s or state()),
+                                      ctypes.byref(t or token()), o, slots, n, nv, split, ws,
+                                      wsb, None)
+
+
+def test_tiled_workspace_size():
+    d = desc()                                          # B=4, H=2, M=16
+    assert D.dl_tiled_workspace_bytes(d, 4) == 4 * 2 * 2 * 15 * 4
+    assert D.dl_tiled_workspace_bytes(d, 0) == 0
+    assert D.dl_tiled_workspace_bytes(desc(merge_interval=1), 4) == 0
+    out = ctypes.c_size_t(0)
+    assert D.lib.dl_tiled_workspace_bytes(ctypes.byref(d), 5, ctypes.byref(out)) == D.DL_E_SHAPE
+    assert D.lib.dl_tiled_workspace_bytes(ctypes.byref(d), 1, None) == D.DL_E_NULL
+
+
+def test_tiled_rejections():
+    """Every tiled-path check fails before any launch (misaligned output last)."""
+    assert tiled(desc(), o=A + 4) == D.DL_E_ALIGN        # everything else valid
+    assert tiled(desc(), nv=3) == D.DL_E_UNSUPPORTED
+    assert tiled(desc(), nv=1) == D.DL_E_UNSUPPORTED
+    assert tiled(desc(state_dtype=D.DL_BF16)) == D.DL_E_DTYPE
+    assert tiled(desc(), ws=None) == D.DL_E_NULL          # split replay needs scratch
+    assert tiled(desc(), ws=A + 8) == D.DL_E_ALIGN
+    assert tiled(desc(), wsb=4 * 2 * 2 * 15 * 4 - 1) == D.DL_E_SHAPE
+    assert tiled(desc(), wsb=4 * 2 * 2 * 15 * 4, o=A + 4) == D.DL_E_ALIGN   # exactly enough
+    assert tiled(desc(), split=0, ws=None, wsb=0, o=A + 4) == D.DL_E_ALIGN  # fused: no scratch
+    assert tiled(desc(merge_interval=1), ws=None, wsb=0, o=A + 4) == D.DL_E_ALIGN
+    assert tiled(desc(), n=0, nv=4, ws=None) == D.DL_OK   # n == 0: no-op
+    assert tiled(desc(), s=state(len=None)) == D.DL_E_NULL
+    assert tiled(desc(), t=token(beta=None)) == D.DL_E_NULL
