@@ -79,6 +79,9 @@ def parse():
     ap.add_argument("--fused-replay", action="store_true",
                     help="with --tiled: every tile recomputes the replay coefficients "
                          "(default: split replay, prepared once per head)")
+    ap.add_argument("--graph", action="store_true",
+                    help="submit the timed steps as replays of one HIP graph holding 16 steps "
+                         "x R launches (the same launches, captured once)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--decode-loop", default="", metavar="MODES",
@@ -381,15 +384,42 @@ def main():
                     events[i][1].record(stream)
                 i += 1
 
+    def with_stream(argtab, handle):
+        return [[a[:-1] + (handle,) for a in row] for row in argtab]
+
     def timed(fn, argtab):
         """W untimed steps, then K timed steps bracketed by synchronize + HIP events on
-        the launch stream; returns elapsed ms (no per-launch events inside)."""
-        run(fn, argtab, 0, WU)
+        the launch stream; returns elapsed ms (no per-launch events inside).  With
+        --graph the steps are replays of one captured graph of POOL steps."""
+        if not args.graph:
+            run(fn, argtab, 0, WU)
+            torch.cuda.synchronize()
+            t0 = torch.cuda.Event(enable_timing=True)
+            t1 = torch.cuda.Event(enable_timing=True)
+            t0.record(stream)
+            run(fn, argtab, WU, K)
+            t1.record(stream)
+            torch.cuda.synchronize()
+            return t0.elapsed_time(t1)
+        if K % POOL or WU % POOL:
+            raise SystemExit(f"--graph needs --steps and --warmup to be multiples of {POOL}")
+        run(fn, argtab, 0, POOL)                    # load the kernels before capture
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        cs = torch.cuda.Stream()
+        cs.wait_stream(stream)
+        with torch.cuda.stream(cs):
+            with torch.cuda.graph(g, stream=cs):
+                run(fn, with_stream(argtab, cs.cuda_stream), 0, POOL)
+        stream.wait_stream(cs)
+        for _ in range(max(WU // POOL - 1, 0)):
+            g.replay()
         torch.cuda.synchronize()
         t0 = torch.cuda.Event(enable_timing=True)
         t1 = torch.cuda.Event(enable_timing=True)
         t0.record(stream)
-        run(fn, argtab, WU, K)
+        for _ in range(K // POOL):
+            g.replay()
         t1.record(stream)
         torch.cuda.synchronize()
         return t0.elapsed_time(t1)
