@@ -4,7 +4,7 @@
 // Thread layout: NCG = dv/4 column groups (one float4 column slice each) times
 // NRG = dk/RPT row groups; every thread keeps RPT rows x 4 columns of the state in
 // registers (rows rg, rg+NRG, ..., so one wave-wide float4 load covers whole
-// consecutive rows, 1 KiB contiguous).  RPT = 16, or 8 for 64 x 64 heads.  The state
+// consecutive rows, 1 KiB contiguous).  RPT = 16, or 4 for 64 x 64 heads.  The state
 // is read from HBM exactly once per step and, when the step materialises (merge /
 // eager / flush), written back exactly once from the same registers -- the read, the
 // key-dimension reductions and the write never leave the workgroup.  Because one
@@ -187,7 +187,15 @@ __device__ __forceinline__ void ld_run(const float* p, float (&o)[N]) {
 }
 template <int N>
 __device__ __forceinline__ void ld_run(const uint16_t* p, float (&o)[N]) {
-  static_assert(N % 8 == 0, "run length");
+  static_assert(N % 4 == 0, "run length");
+  if constexpr (N % 8 != 0) {
+#pragma unroll
+    for (int x = 0; x < N; x += 4) {
+      const uint2 w = *reinterpret_cast<const uint2*>(p + x);
+      o[x + 0] = bf_lo(w.x); o[x + 1] = bf_hi(w.x); o[x + 2] = bf_lo(w.y); o[x + 3] = bf_hi(w.y);
+    }
+    return;
+  }
 #pragma unroll
   for (int x = 0; x < N; x += 8) {
     const uint4 w = *reinterpret_cast<const uint4*>(p + x);
@@ -239,18 +247,29 @@ template <int N> struct RawRun<float, N> {
   }
 };
 template <int N> struct RawRun<uint16_t, N> {
-  uint4 w[N / 8];
+  static_assert(N % 4 == 0, "run length");
+  static constexpr bool W16 = N % 8 == 0;           // 16-byte words, else 8-byte words
+  using Word = std::conditional_t<W16, uint4, uint2>;
+  Word w[W16 ? N / 8 : N / 4];
   __device__ __forceinline__ void load(const uint16_t* p) {
 #pragma unroll
-    for (int i = 0; i < N / 8; ++i) w[i] = reinterpret_cast<const uint4*>(p)[i];
+    for (int i = 0; i < (W16 ? N / 8 : N / 4); ++i) w[i] = reinterpret_cast<const Word*>(p)[i];
   }
   __device__ __forceinline__ void get(float (&o)[N]) const {
+    if constexpr (W16) {
 #pragma unroll
-    for (int i = 0; i < N / 8; ++i) {
-      o[8 * i + 0] = bf_lo(w[i].x); o[8 * i + 1] = bf_hi(w[i].x);
-      o[8 * i + 2] = bf_lo(w[i].y); o[8 * i + 3] = bf_hi(w[i].y);
-      o[8 * i + 4] = bf_lo(w[i].z); o[8 * i + 5] = bf_hi(w[i].z);
-      o[8 * i + 6] = bf_lo(w[i].w); o[8 * i + 7] = bf_hi(w[i].w);
+      for (int i = 0; i < N / 8; ++i) {
+        o[8 * i + 0] = bf_lo(w[i].x); o[8 * i + 1] = bf_hi(w[i].x);
+        o[8 * i + 2] = bf_lo(w[i].y); o[8 * i + 3] = bf_hi(w[i].y);
+        o[8 * i + 4] = bf_lo(w[i].z); o[8 * i + 5] = bf_hi(w[i].z);
+        o[8 * i + 6] = bf_lo(w[i].w); o[8 * i + 7] = bf_hi(w[i].w);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < N / 4; ++i) {
+        o[4 * i + 0] = bf_lo(w[i].x); o[4 * i + 1] = bf_hi(w[i].x);
+        o[4 * i + 2] = bf_lo(w[i].y); o[4 * i + 3] = bf_hi(w[i].y);
+      }
     }
   }
 };
@@ -260,10 +279,10 @@ __device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0
 
 // ------------------------------------------------------------------ configuration
 // Threads per workgroup for a dk x dv head: dv/4 column groups x dk/rows-per-thread
-// row groups.  Small (64 x 64) heads keep 8 rows per thread (two waves per head), the
-// others 16 rows per thread.
+// row groups.  Small (64 x 64) heads keep 4 rows per thread (four waves per head: short
+// per-thread chains for a 16 KiB state), the others 16 rows per thread.
 #ifndef DL_SMALL_HEAD_RPT
-#define DL_SMALL_HEAD_RPT 8
+#define DL_SMALL_HEAD_RPT 4
 #endif
 constexpr int rows_per_thread(int dk, int dv) {
   return (dk == 64 && dv == 64) ? DL_SMALL_HEAD_RPT : 16;
@@ -306,7 +325,7 @@ struct Cfg {
   static_assert(64 % NCG == 0, "a wave must hold whole rows");
   static_assert(NT % LPE == 0 && DK % LPE == 0, "coefficient pass layout");
   static_assert(NT >= DK, "one thread per key row in the prologue");
-  static_assert(RPL == 8 || RPL == 16, "coefficient pass run length");
+  static_assert(RPL == 4 || RPL == 8 || RPL == 16, "coefficient pass run length");
   static_assert(CH == EPP, "the first merge chunk is staged by the first coefficient pass");
   static_assert(LPE <= 64 && 64 % LPE == 0, "an entry's lanes share one wave");
   static_assert(NT == threads_per_head(DK, DV), "launch bound must match the layout");
@@ -318,11 +337,15 @@ struct Cfg {
 template <int OP, typename TIN>
 struct UType { using type = std::conditional_t<OpTraits<OP>::DELTA, float, TIN>; };
 
-#if DL_WAVES_PER_EU > 0
-#define DL_OCCUPANCY __attribute__((amdgpu_waves_per_eu(DL_WAVES_PER_EU)))
-#else
-#define DL_OCCUPANCY
+// Occupancy target (waves per SIMD) for the register allocator: DL_WAVES_PER_EU for every
+// kernel if set, else DL_SMALL_HEAD_WAVES for 64 x 64 heads (1 = no target).
+#ifndef DL_SMALL_HEAD_WAVES
+#define DL_SMALL_HEAD_WAVES 6
 #endif
+constexpr int waves_target(int dk, int dv) {
+  return DL_WAVES_PER_EU > 0 ? DL_WAVES_PER_EU : ((dk == 64 && dv == 64) ? DL_SMALL_HEAD_WAVES : 1);
+}
+#define DL_OCCUPANCY __attribute__((amdgpu_waves_per_eu(waves_target(DK, DV))))
 
 // ------------------------------------------------------------------ the kernel
 // Every global load a workgroup needs is issued before its first barrier: the token
@@ -451,7 +474,7 @@ void deltalog_kernel(KParams p) {
   const int e_ = tid / CF::LPE;                   // coefficient pass: entry within the pass
   const int c_ = tid % CF::LPE;                   //                   key-row run
   // Per-key snapshots are prefetched only where the registers allow it (small heads).
-  constexpr bool kPrefetchPerKey = DL_PREFETCH_PER_KEY || (DL_PREFETCH_PER_KEY_SMALL && RPT == 8);
+  constexpr bool kPrefetchPerKey = DL_PREFETCH_PER_KEY || (DL_PREFETCH_PER_KEY_SMALL && RPT <= 8);
   float kr[RPL], lr_[(DL == 1) ? 1 : RPL];
   RawRun<TIN, RPL> kr_raw{};
   RawRun<float, (DL == 1) ? 8 : RPL> lr_raw{};      // per-key snapshots (unused for DL == 1)
