@@ -53,7 +53,7 @@
 extern "C" {
 #endif
 
-#define DL_ABI_VERSION 2
+#define DL_ABI_VERSION 3
 #define DL_MAX_MERGE_INTERVAL 64
 
 typedef enum {
@@ -112,6 +112,7 @@ typedef struct {
   void*    k_log;    /* [B,H,C,dk]  in_dtype   key-side factors   (may be NULL if C == 0) */
   void*    u_log;    /* [B,H,C,dv]  u_log_dtype value-side factors (may be NULL if C == 0)*/
   float*   lam_log;  /* [B,H,C,dl]  fp32 snapshot of ell per entry (may be NULL if C == 0)*/
+                     /*             for dl == 1 stored entry-major, [B,C,H]               */
                      /*             (ignored, may be NULL, for LINATTN)                  */
   int32_t* len;      /* [B,H]       live-log length L in [0, C]                          */
   int32_t* err;      /* [1]         sticky device error word (see above); may be NULL    */

@@ -274,6 +274,21 @@ template <int N> struct RawRun<uint16_t, N> {
   }
 };
 
+// Lam_log addressing.  Per-key snapshots of a (slot, head) are contiguous rows of dk
+// values, [B,H,C,dk].  Scalar snapshots are stored entry-major, [B,C,H]: the H heads of a
+// slot append entry L side by side (one 128-byte line for 32 heads) instead of each
+// writing 4 bytes into a sector of its own.  Entry i of a (slot, head) is at
+// base[i * stride].
+template <int DL>
+__device__ __forceinline__ float* lam_log_base(const KParams& p, int slot, int h) {
+  if constexpr (DL == 1) return p.lam_log + size_t(slot) * size_t(p.C) * p.H + h;
+  else return p.lam_log + (size_t(slot) * p.H + h) * size_t(p.C) * DL;
+}
+template <int DL>
+__device__ __forceinline__ size_t lam_log_stride(const KParams& p) {
+  return DL == 1 ? size_t(p.H) : size_t(DL);
+}
+
 // Nothing may be scheduled across this point (loads keep their issue order).
 __device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
 
@@ -469,7 +484,9 @@ void deltalog_kernel(KParams p) {
   }
 
   const TIN* Kb = static_cast<const TIN*>(p.k_log) + sh * size_t(C) * DK;
-  const float* Lb = CF::DECAY ? p.lam_log + sh * size_t(C) * DL : nullptr;
+  float* const Lw = CF::DECAY ? lam_log_base<DL>(p, slot, h) : nullptr;
+  const float* Lb = Lw;
+  const size_t LS = lam_log_stride<DL>(p);
   const TU* Ub = static_cast<const TU*>(p.u_log) + sh * size_t(C) * DV;
   const int e_ = tid / CF::LPE;                   // coefficient pass: entry within the pass
   const int c_ = tid % CF::LPE;                   //                   key-row run
@@ -491,7 +508,7 @@ void deltalog_kernel(KParams p) {
     const int ek = min(e_, Lm1);
     kr_raw.load(Kp + size_t(ek) * DK + c_ * RPL);
     if constexpr (DL == 1) {
-      if constexpr (CF::DECAY) lr0 = Lp[ek];
+      if constexpr (CF::DECAY) lr0 = Lp[size_t(ek) * LS];
     } else {
       lr_raw.load(Lp + size_t(ek) * DK + c_ * RPL);
     }
@@ -569,7 +586,7 @@ void deltalog_kernel(KParams p) {
         if (i0 > 0 || !DL_PREFETCH_KEYS || (DL != 1 && !kPrefetchPerKey)) {
           ld_run<RPL>(Kb + size_t(i) * DK + c_ * RPL, kr);
           if constexpr (DL == 1) {
-            if constexpr (CF::DECAY) lr_[0] = Lb[i];
+            if constexpr (CF::DECAY) lr_[0] = Lb[size_t(i) * LS];
           } else {
             ld_run<RPL>(Lb + size_t(i) * DK + c_ * RPL, lr_);
           }
@@ -713,7 +730,7 @@ void deltalog_kernel(KParams p) {
         reinterpret_cast<uint4*>(Kd)[x] = reinterpret_cast<const uint4*>(kin)[x];
       if constexpr (CF::DECAY) {
         for (int x = tid; x < DL; x += NT) {
-          p.lam_log[ent * DL + x] = s_lm[x];
+          Lw[size_t(L) * LS + x] = s_lm[x];
           p.ell[sh * DL + x] = s_lm[x];
         }
       }
@@ -744,7 +761,7 @@ void deltalog_kernel(KParams p) {
             const int i = i0 + ii;
             val = ld1(Kb + size_t(i) * DK + r);
             if constexpr (CF::DECAY) {
-              const float lam_i = Lb[size_t(i) * DL + ((DL == 1) ? 0 : r)];
+              const float lam_i = Lb[size_t(i) * LS + ((DL == 1) ? 0 : r)];
               val *= dl_exp(s_lm[(DL == 1) ? 0 : r] - lam_i);
             }
           }

@@ -47,8 +47,8 @@ struct TileCfg {
 // Every entry is reduced by 16 lanes of dk/16 rows each, whatever the workgroup size, so
 // every caller produces the same bits.  Results go to gk[i], gq[i] (i < L).
 template <int OP, int DK, int NT, typename TIN, typename Sink>
-__device__ __forceinline__ void replay_coefficients(const TIN* Kb, const float* Lb, int L,
-                                                    const float* s_kf, const float* s_qf,
+__device__ __forceinline__ void replay_coefficients(const TIN* Kb, const float* Lb, size_t LS,
+                                                    int L, const float* s_kf, const float* s_qf,
                                                     const float* s_lr, Sink sink) {
   using TR = OpTraits<OP>;
   constexpr int DL = TR::PER_KEY ? DK : 1;
@@ -63,12 +63,12 @@ __device__ __forceinline__ void replay_coefficients(const TIN* Kb, const float* 
       for (int x = 0; x < RPL; ++x) {
         const int r = c_ * RPL + x;
         float kr = ld1(Kb + size_t(i) * DK + r);
-        if constexpr (TR::DECAY && DL != 1) kr *= dl_exp(s_lr[r] - Lb[size_t(i) * DK + r]);
+        if constexpr (TR::DECAY && DL != 1) kr *= dl_exp(s_lr[r] - Lb[size_t(i) * LS + r]);
         ak = fmaf(kr, s_kf[r], ak);
         aq = fmaf(kr, s_qf[r], aq);
       }
       if constexpr (TR::DECAY && DL == 1) {
-        const float w = dl_exp(s_lr[0] - Lb[i]);
+        const float w = dl_exp(s_lr[0] - Lb[size_t(i) * LS]);
         ak *= w;
         aq *= w;
       }
@@ -118,8 +118,10 @@ __global__ __launch_bounds__(256) void replay_prep_kernel(KParams p, float* coef
   __syncthreads();
   const int C = p.C;
   float* out = coef + th * 2 * size_t(C);
+  const int slot = int(sh / size_t(p.H));
   replay_coefficients<OP, DK, 256>(static_cast<const TIN*>(p.k_log) + sh * size_t(C) * DK,
-                                   TR::DECAY ? p.lam_log + sh * size_t(C) * DL : nullptr, L,
+                                   TR::DECAY ? lam_log_base<DL>(p, slot, h) : nullptr,
+                                   lam_log_stride<DL>(p), L,
                                    s_kf, s_qf, s_lr, [&](int i, float gk, float gq) {
                                      out[i] = gk;
                                      out[C + i] = gq;
@@ -224,7 +226,9 @@ void tile_step_kernel(KParams p, const float* __restrict__ coef) {
   float beta = 0.f;
   if constexpr (TR::DELTA) beta = p.beta[th];
   const TIN* Kb = static_cast<const TIN*>(p.k_log) + sh * size_t(C) * DK;
-  const float* Lb = TR::DECAY ? p.lam_log + sh * size_t(C) * DL : nullptr;
+  float* const Lw = TR::DECAY ? lam_log_base<DL>(p, slot, h) : nullptr;
+  const float* Lb = Lw;
+  const size_t LS = lam_log_stride<DL>(p);
   const TU* Ub = static_cast<const TU*>(p.u_log) + sh * size_t(C) * DV;
   __syncthreads();
 
@@ -236,7 +240,7 @@ void tile_step_kernel(KParams p, const float* __restrict__ coef) {
       s_gq[i] = cp[C + i];
     }
   } else {
-    replay_coefficients<OP, DK, NT>(Kb, Lb, L, s_kf, s_qf, s_lr, [&](int i, float gk, float gq) {
+    replay_coefficients<OP, DK, NT>(Kb, Lb, LS, L, s_kf, s_qf, s_lr, [&](int i, float gk, float gq) {
       s_gk[i] = gk;
       s_gq[i] = gq;
     });
@@ -304,7 +308,7 @@ void tile_step_kernel(KParams p, const float* __restrict__ coef) {
       for (int x = tid; x < KCH; x += NT)
         reinterpret_cast<uint4*>(Kd)[x] = reinterpret_cast<const uint4*>(kin)[x];
       if constexpr (TR::DECAY)
-        for (int x = tid; x < DL; x += NT) p.lam_log[ent * DL + x] = s_lm[x];
+        for (int x = tid; x < DL; x += NT) Lw[size_t(L) * LS + x] = s_lm[x];
     }
     return;                                        // ell and L: finalize_kernel
   }
@@ -326,7 +330,7 @@ void tile_step_kernel(KParams p, const float* __restrict__ coef) {
         const int i = i0 + ii;
         val = ld1(Kb + size_t(i) * DK + r);
         if constexpr (TR::DECAY)
-          val *= dl_exp(s_lm[DL == 1 ? 0 : r] - Lb[size_t(i) * DL + (DL == 1 ? 0 : r)]);
+          val *= dl_exp(s_lm[DL == 1 ? 0 : r] - Lb[size_t(i) * LS + (DL == 1 ? 0 : r)]);
       }
       s_kt[r * KTS + ii] = val;                     // K~_i[r] = e^(l'_r - Lam_i,r) K_i[r]
     }

@@ -27,7 +27,7 @@ if not os.path.exists(LIB_PATH):
 _lib = ctypes.CDLL(LIB_PATH)
 
 # ----------------------------------------------------------------- constants (deltalog.h)
-DL_ABI_VERSION = 2
+DL_ABI_VERSION = 3
 DL_MAX_MERGE_INTERVAL = 64
 DL_OK, DL_E_NULL, DL_E_SHAPE, DL_E_DTYPE, DL_E_ALIGN, DL_E_UNSUPPORTED, DL_E_HIP, DL_E_VERSION = (
     0, -1, -2, -3, -4, -5, -6, -7)
@@ -166,7 +166,11 @@ class DeltaLogState:
         self.ell = torch.zeros((B, H, dl), **f32) if dl else None
         self.k_log = torch.zeros((B, H, max(C, 0), dk), dtype=in_t, device=device)
         self.u_log = torch.zeros((B, H, max(C, 0), dv), dtype=u_t, device=device)
-        self.lam_log = torch.zeros((B, H, max(C, 0), dl), **f32) if dl else None
+        # scalar snapshots are entry-major [B, C, H] (the heads of a slot side by side)
+        if dl == 1:
+            self.lam_log = torch.zeros((B, max(C, 0), H), **f32)
+        else:
+            self.lam_log = torch.zeros((B, H, max(C, 0), dl), **f32) if dl else None
         self.len = torch.zeros((B, H), dtype=torch.int32, device=device)
         self.err = torch.zeros((1,), dtype=torch.int32, device=device)
         self.struct = dl_state(_ptr(self.S), _ptr(self.ell),

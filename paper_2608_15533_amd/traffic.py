@@ -99,10 +99,12 @@ def amortized_bytes_per_token(op, dk, dv, M, in_dtype="bf16", state_dtype="f32")
     return c.total / M
 
 
-def state_write_ratio(op, dk, dv, M, in_dtype="bf16", state_dtype="f32"):
-    """Eager / DeltaLog state-write bytes per token, outputs excluded: M / (1 + eps)."""
+def state_write_ratio(op, dk, dv, M, in_dtype="bf16", state_dtype="f32", live_length_bytes=0):
+    """Eager / DeltaLog state-write bytes per token, outputs excluded: M / (1 + eps).
+    ``live_length_bytes`` adds the per-step write of the live length (metadata the model
+    of Eq. 9 omits; 4 for the int32 length this library keeps per slot and head)."""
     _, state, entry, decay, _ = _sizes(op, dk, dv, in_dtype, state_dtype)
-    dl_writes = (state + (M - 1) * entry + M * decay) / M
+    dl_writes = (state + (M - 1) * entry + M * (decay + live_length_bytes)) / M
     return state / dl_writes
 
 

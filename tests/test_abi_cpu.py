@@ -36,7 +36,7 @@ def test_header_functions_are_exported():
 
 
 def test_version_and_status_strings():
-    assert D.dl_abi_version() == D.DL_ABI_VERSION == 2
+    assert D.dl_abi_version() == D.DL_ABI_VERSION == 3
     for code in range(0, -8, -1):
         s = D.dl_status_str(code)
         assert s.startswith("DL_") and s != "unknown dl_status"

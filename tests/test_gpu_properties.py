@@ -215,7 +215,10 @@ def test_log_contents_match_the_model(op):
     if op == "linattn":
         assert "lam_log" not in a and "ell" not in a
     else:
-        assert rel(a["lam_log"].reshape(N, M - 1, -1)[:, :L], model.Lam[:, :L]) <= 1e-6
+        lam_log = a["lam_log"]
+        if lam_log.ndim == 3:               # scalar snapshots: entry-major [B, C, H]
+            lam_log = lam_log.transpose(0, 2, 1)[..., None]
+        assert rel(lam_log.reshape(N, M - 1, -1)[:, :L], model.Lam[:, :L]) <= 1e-6
         assert rel(a["ell"].reshape(N, -1), model.ell) <= 1e-6
     U = a["u_log"].astype(np.float64).reshape(N, M - 1, w.dv)[:, :L]
     if op not in OE.DELTA_OPS:

@@ -77,3 +77,13 @@ def test_byte_optimal_merge_interval():
         a = [T.amortized_bytes_per_token(op, d, d, M) for M in range(1, 65)]
         assert a[m - 1] == min(a)
         assert a[m - 1] < T.eager_bytes(op, d, d).total
+
+
+def test_live_length_metadata_lowers_the_write_ratio_slightly():
+    """The int32 live length written every step is metadata outside Eq. 9; including it
+    lowers the implied write reduction by well under 1% at the tested shapes."""
+    for op, d, M in (("gdn", 128, 16), ("kda", 128, 16), ("rwkv6", 64, 16)):
+        base = T.state_write_ratio(op, d, d, M)
+        with_len = T.state_write_ratio(op, d, d, M, live_length_bytes=4)
+        assert with_len < base
+        assert (base - with_len) / base < 0.01
