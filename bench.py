@@ -149,6 +149,29 @@ def counter_traffic(key):
     return d["step_kernel_bytes_per_launch"], os.path.relpath(path, ROOT)
 
 
+def copy_ceiling(torch, stream, gib=2, reps=5):
+    """Read+write GB/s of the runtime's device-to-device copy of ``gib`` GiB (median of
+    ``reps`` copies timed with HIP events on the launch stream), reported beside the
+    kernel's achieved bandwidth as a reference point for read-and-write traffic."""
+    n = (gib << 30) // 4
+    src = torch.empty(n, dtype=torch.float32, device="cuda").fill_(1.0)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    ms = []
+    for _ in range(reps):
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        dst.copy_(src)
+        b.record(stream)
+        torch.cuda.synchronize()
+        ms.append(a.elapsed_time(b))
+    del src, dst
+    torch.cuda.empty_cache()
+    return 2 * (gib << 30) / (float(np.median(ms)) * 1e-3) / 1e9
+
+
 def cpu_baseline(w, budget_s):
     """The fp64 oracle eager recurrence, as it stands, on a bounded sample of the same
     workload shape (the B x H heads of one layer -- at most 64 x 32 x 128^2 -- for as
@@ -488,6 +511,7 @@ def main():
 
     traffic, traffic_src = counter_traffic(profile_key(args.workload, sd, args.tiled,
                                                        args.fused_replay))
+    copy_gbs = copy_ceiling(torch, stream)
     state_mib = heads * w.dk * w.dv * (2 if sd == "bf16" else 4) / 2**20
     kname = {"gdn": "GDN", "kda": "KDA", "rwkv6": "RWKV6", "linattn": "LinearAttention",
              "retnet": "RetNet", "gla": "GLA"}[w.op]
@@ -540,6 +564,8 @@ def main():
             "traffic_unit": "bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
             "traffic_source": traffic_src,
             "avg_launch_us": round(avg_launch_us, 3),
+            "d2d_copy_GB/s": round(copy_gbs, 1),
+            "achieved_vs_d2d_copy": round(achieved / copy_gbs, 4),
             "algorithmic_bytes_per_launch": round(bytes_per_launch, 1),
             "duration_source": "HIP events around the timed region / launches",
         },

@@ -375,3 +375,78 @@ def test_exact_dyadic_bf16_state_bitwise(op):
     for t in range(steps):
         np.testing.assert_array_equal(eo[t].astype(np.float64), ref_o[t], err_msg=f"eager {t}")
     np.testing.assert_array_equal(eS.float().cpu().numpy().astype(np.float64), ref_S[-1])
+
+
+@pytest.mark.parametrize("M", [2, 8])
+@pytest.mark.parametrize("op", OPS)
+def test_embedded_2x2_bruteforce(op, M):
+    """The 2x2 exact-rational brute force of the oracle pins, embedded in a 64x64 head
+    (state, keys, queries and values zero outside the 2x2 block, so the block evolves
+    exactly as the hand-expanded formulas say): three steps through dl_append_step (M = 2
+    merges at the second step; M = 8 only appends) and a flush.  Inputs are stored in
+    fp32 and the exact reference uses the stored values; the decay goes through the
+    hardware exp, hence a 1e-6 bar inside the block and exact zeros outside it."""
+    from fractions import Fraction as Fr
+
+    import oracle_pins as P
+
+    d = 64
+    S = [[Fr(1, 2), Fr(-3, 4)], [Fr(5, 8), Fr(1, 4)]]
+    seq = [
+        dict(q=[Fr(3, 5), Fr(4, 5)], k=[Fr(4, 5), Fr(-3, 5)], v=[Fr(1), Fr(-2)],
+             beta=Fr(1, 2), g=[Fr(3, 4), Fr(1, 2)]),
+        dict(q=[Fr(-1, 2), Fr(1, 3)], k=[Fr(1, 3), Fr(2, 3)], v=[Fr(3, 2), Fr(1, 4)],
+             beta=Fr(3, 4), g=[Fr(7, 8), Fr(5, 8)]),
+        dict(q=[Fr(2), Fr(-1)], k=[Fr(-1, 2), Fr(1, 2)], v=[Fr(-1), Fr(1, 8)],
+             beta=Fr(1, 4), g=[Fr(1, 2), Fr(15, 16)]),
+    ]
+    u2 = [Fr(1, 5), Fr(-2, 5)]
+    f32 = lambda x: np.float32(float(x))
+    exact = lambda x: Fr(float(np.float32(x)))          # the stored fp32 value, exactly
+    S0 = np.zeros((1, 1, d, d), np.float32)
+    for i in range(2):
+        for j in range(2):
+            S0[0, 0, i, j] = f32(S[i][j])
+    S = [[exact(S0[0, 0, i, j]) for j in range(2)] for i in range(2)]
+    u = None
+    if op == "rwkv6":
+        u = np.zeros((1, d), np.float32)
+        u[0, :2] = [f32(x) for x in u2]
+        u2 = [exact(x) for x in u[0, :2]]
+    scalar = op in ("gdn", "retnet", "linattn")
+    xs, refs = [], []
+    for st in seq:
+        g = [Fr(1), Fr(1)] if op == "linattn" else ([st["g"][0]] * 2 if scalar else st["g"])
+        x = {n: np.zeros((1, 1, d), np.float32) for n in ("q", "k", "v")}
+        for n in ("q", "k", "v"):
+            x[n][0, 0, :2] = [f32(t) for t in st[n]]
+        lam_vals = [np.float32(np.log(float(t))) for t in g]
+        if op == "linattn":
+            x["lam"] = None
+        elif scalar:
+            x["lam"] = np.array([[lam_vals[0]]], np.float32)
+        else:
+            x["lam"] = np.zeros((1, 1, d), np.float32)
+            x["lam"][0, 0, :2] = lam_vals
+        x["beta"] = np.array([[f32(st["beta"])]], np.float32) if op in OE.DELTA_OPS else None
+        xs.append(x)
+        # exact recurrence on the stored inputs; the decay factor is exp of the stored
+        # lambda, taken as the nearest rational (the only non-exact quantity)
+        ge = [Fr(float(np.exp(np.float64(v)))) for v in lam_vals] if op != "linattn" else g
+        q2, k2, v2 = ([exact(t) for t in x[n][0, 0, :2]] for n in ("q", "k", "v"))
+        b2 = exact(x["beta"][0, 0]) if x["beta"] is not None else None
+        S, o = P._bf_step_fraction(op, S, q2, k2, v2, b2, ge, u2)
+        refs.append(([float(t) for t in o], [[float(t) for t in row] for row in S]))
+    desc = D().make_desc(op, 1, 1, d, d, M, "f32")
+    outs, st = run_deltalog(desc, S0, xs, u)
+    for t, (o_ref, _) in enumerate(refs):
+        np.testing.assert_allclose(outs[t][0, 0, :2], o_ref, rtol=1e-6, atol=1e-6,
+                                   err_msg=f"{op} M={M} step {t}")
+        assert not np.any(outs[t][0, 0, 2:]), f"{op} output outside the block, step {t}"
+    D().dl_merge(desc, st)
+    torch.cuda.synchronize()
+    Sg = st.S.cpu().numpy()[0, 0]
+    np.testing.assert_allclose(Sg[:2, :2], refs[-1][1], rtol=1e-6, atol=1e-6,
+                               err_msg=f"{op} M={M} flushed block")
+    Sg[:2, :2] = 0.0
+    assert not np.any(Sg), f"{op} M={M}: state outside the block"
