@@ -93,6 +93,11 @@ def parse():
                     help="decode loop, fused mode: rows of merging slots first (default: slot order)")
     ap.add_argument("--uniform", action="store_true",
                     help="decode loop: admit every sequence at once (default: staggered)")
+    ap.add_argument("--autotune", type=int, default=0, metavar="MAX_M",
+                    help="instead of the kernel bench: measure the append cost at every live "
+                         "length and the merge cost at every length up to MAX_M, predict the "
+                         "amortised step time of every merge interval, and check the "
+                         "prediction against timed cycles")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (5 times); used to "
                          "scale the HBM byte counters of a profiler run")
@@ -308,6 +313,78 @@ def decode_loop(args):
     }), flush=True)
 
 
+def autotune(args):
+    """Merge-interval selection from measured phase costs for the chosen workload shape
+    (``--batch`` and ``--state-dtype`` apply), checked against timed full cycles at
+    several merge intervals.  Prints one JSON line."""
+    import torch
+    from paper_2608_15533_amd import autotune as A
+    from paper_2608_15533_amd import deltalog as D
+    from paper_2608_15533_amd import traffic as T
+
+    w, _ = workloads()[args.workload]
+    if args.batch:
+        w = w.with_(B=args.batch)
+    sd = args.state_dtype
+    max_M = args.autotune
+    torch.cuda.set_device(0)
+    t0 = time.perf_counter()
+    cal = A.calibrate(w.op, w.B, w.H, w.dk, w.dv, w.in_dtype, sd, max_M=max_M, reps=5)
+    cal_s = time.perf_counter() - t0
+    best, pred = A.choose(cal["append_us"], cal["merge_us"])
+    R = cal["replicas"]
+
+    def cycle_us(M, cycles=4):
+        """Mean launch time of dl_append_step over whole M-step cycles (every slot at
+        the same live length, R layer states in turn)."""
+        desc = D.make_desc(w.op, w.B, w.H, w.dk, w.dv, M, w.in_dtype, sd)
+        gen = torch.Generator(device="cuda")
+        gen.manual_seed(7)
+        sts = [D.DeltaLogState(desc, 0.02 * torch.randn(w.B, w.H, w.dk, w.dv, generator=gen,
+                                                        device="cuda")) for _ in range(R)]
+        tok = A._token(desc, w.B, gen)
+        o = torch.empty((w.B, w.H, w.dv), dtype=torch.float32, device="cuda")
+        for _ in range(M):
+            for st in sts:
+                D.dl_append_step(desc, st, tok, o)
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(cycles * M):
+            for st in sts:
+                D.dl_append_step(desc, st, tok, o)
+        e1.record()
+        e1.synchronize()
+        assert all(int(st.err.item()) == 0 for st in sts)
+        us = e0.elapsed_time(e1) * 1e3 / (cycles * M * R)
+        del sts
+        torch.cuda.empty_cache()
+        return us
+
+    check = sorted({M for M in (1, 2, 4, 8, 16, 32, 64, best) if M <= max_M})
+    measured = {M: cycle_us(M) for M in check}
+    mbest = min(measured, key=lambda M: (measured[M], M))
+    res = {
+        "autotune": {
+            "workload": w.name, "op": w.op, "batch": w.B, "heads": w.H, "dk": w.dk,
+            "dv": w.dv, "in_dtype": w.in_dtype, "state_dtype": sd, "replicas": R,
+            "calibration_s": round(cal_s, 2),
+            "append_us": [round(x, 3) for x in cal["append_us"]],
+            "merge_us": [round(x, 3) for x in cal["merge_us"]],
+            "predicted_us_per_step": {M: round(t, 3) for M, t in pred.items()},
+            "chosen_M": best,
+            "byte_optimal_M": T.byte_optimal_merge_interval(w.op, w.dk, w.dv, w.in_dtype, sd,
+                                                            max_M=max_M),
+            "measured_us_per_step": {M: round(t, 3) for M, t in measured.items()},
+            "measured_best_M_of_checked": mbest,
+            "chosen_vs_measured_best": round(measured[best] / measured[mbest], 4),
+            "predicted_tokens_per_s": round(w.B * 1e6 / pred[best], 1),
+            "measured_tokens_per_s_at_chosen": round(w.B * 1e6 / measured[best], 1),
+        }
+    }
+    print(json.dumps(res), flush=True)
+
+
 def main():
     args = parse()
     if args.copy_calibration:
@@ -319,6 +396,9 @@ def main():
         sys.exit(2)
     if args.decode_loop:
         decode_loop(args)
+        return
+    if args.autotune:
+        autotune(args)
         return
 
     import ctypes
