@@ -349,6 +349,7 @@ def autotune(args):
                 D.dl_append_step(desc, st, tok, o)
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(200_000)           # the host enqueues while the device is busy
         e0.record()
         for _ in range(cycles * M):
             for st in sts:

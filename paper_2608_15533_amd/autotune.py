@@ -76,6 +76,10 @@ def _timed(launch, states, reps, prepare):
     for _ in range(reps):
         for st in states:
             prepare(st)
+        # Keep the device busy while the host enqueues the timed launches, so that the
+        # interval holds launches only, not the host's submission time.
+        if hasattr(torch.cuda, "_sleep"):
+            torch.cuda._sleep(50_000 * len(states))
         e0.record()
         for st in states:
             launch(st)
