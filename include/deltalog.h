@@ -1,6 +1,7 @@
 /*
  * deltalog.h -- C ABI of libdeltalog.so: DeltaLog one-token decode state update for
- * gated linear attention (GDN, KDA, RWKV6) on AMD Instinct MI355X (gfx950).
+ * linear-attention recurrences (the Table 1 operators: GDN, KDA, RWKV6, linear
+ * attention, RetNet, GLA) on AMD Instinct MI355X (gfx950).
  *
  * The method (deferred materialisation of recurrent states, Sec. 3): the dense
  * recurrent state of each (slot, head) is kept as a dense base S plus a bounded log of
@@ -22,7 +23,8 @@
  *    stream has executed it.  Calls on distinct buffers are re-entrant and thread-safe.
  *  - Arrays are dense, row-major, with the shapes given below.  B = desc->num_slots,
  *    H = desc->heads, C = desc->merge_interval - 1 (live-log capacity),
- *    dl = 1 for GDN (one log-decay per head) and dl = dk for KDA/RWKV6 (per key).
+ *    dl = 1 for GDN and RetNet (one log-decay per head), dl = dk for KDA, RWKV6 and
+ *    GLA (per key); linear attention has no decay (no ell, lam_log or lam).
  *  - The state matrix of a head is dk x dv, rows indexed by the key dimension; the
  *    decay D(.) scales rows (Eq. 2); outputs are o = x^T S (length dv).
  *  - `slots` is a device int32 array of n distinct slot ids in [0, B): token row i
