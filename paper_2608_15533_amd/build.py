@@ -59,5 +59,28 @@ def build(verbose=False, extra_flags=()):
     return LIB
 
 
+C_EXAMPLE_SRC = os.path.join(ROOT, "tests", "c_abi", "dl_example.c")
+C_EXAMPLE_LIB = os.path.join(ROOT, "tests", "c_abi", "libdl_example.so")
+
+
+def build_c_example(verbose=False):
+    """Compile the pure-C ABI example (tests/c_abi/dl_example.c) with the host C compiler
+    into a shared library linked against libdeltalog.so (found next to it at run time
+    through the rpath).  The GPU tests load it with ctypes."""
+    rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
+    rpath = os.path.relpath(PKG, os.path.dirname(C_EXAMPLE_LIB))
+    cmd = ["gcc", "-std=c11", "-O2", "-fPIC", "-shared", "-Wall", "-Werror",
+           "-D__HIP_PLATFORM_AMD__", "-I", INCLUDE, "-I", os.path.join(rocm, "include"),
+           C_EXAMPLE_SRC, "-o", C_EXAMPLE_LIB, "-L", PKG, "-ldeltalog",
+           "-L", os.path.join(rocm, "lib"), "-lamdhip64", "-lm",
+           f"-Wl,-rpath,$ORIGIN/{rpath}", f"-Wl,-rpath,{os.path.join(rocm, 'lib')}"]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"C example build failed:\n{' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
+    if verbose:
+        print(f"built {C_EXAMPLE_LIB}")
+    return C_EXAMPLE_LIB
+
+
 if __name__ == "__main__":
     build(verbose=True, extra_flags=sys.argv[1:])
