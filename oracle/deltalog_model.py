@@ -26,7 +26,7 @@ line; ``replay_readout`` additionally writes the readout directly in factored fo
 quantity a kernel computes without materialising S) and is pinned against the dense
 readout in the tests.
 
-Readings (listed in the design doc): the delta-rule correction is taken on the decayed
+Readings: the delta-rule correction is taken on the decayed
 state D(lambda_t) S_{t-1}, which is Eq. 7 evaluated at the already-advanced ``ell``;
 the merging step is the M-th step of a cycle and consumes that step's token (Eq. 6
 includes a_t b_t^T); merge and flush are also defined at any live length L < C, since

@@ -16,7 +16,7 @@ instantiates (a_t, b_t) and the decay form per operator:
     RetNet   : head-wise scalar decay gamma_t = exp(lambda_t), a = k, b = v
     GLA      : per-key (diagonal) decay, a = k, b = v
 
-Readings taken where the text is silent or ambiguous (each is listed in the design doc):
+Readings taken where the text is silent or ambiguous:
 
 * Correction state (delta rule).  Table 1 writes the old-state correction as
   ``k_t^T S_{t-1}``.  The paper states the model semantics are unchanged and that the

@@ -7,7 +7,7 @@ library is tested and benchmarked on.  It is the only code shared by the HIP pat
 tests/bench and the CPU oracle's tests: it draws random numbers and rounds them to the
 storage dtype, nothing else.
 
-Recipe (also stated in the design doc):
+Recipe:
 
 * Seeds: ``numpy.random.default_rng([20261202, cfg, layer, stream, idx])`` with
   stream 0 = initial state (idx = slot), 1 = step inputs (idx = step t; warm-up steps
