@@ -126,3 +126,17 @@ def test_long_rollout_no_drift(op, w, M):
         + ", ".join(f"{e:.1e}" for e in errs))
     _check(r, f"{op} long rollout M={M} x 64 cycles")
     assert errs[-1] <= 10 * max(errs[0], 1e-7), errs
+
+
+@pytest.mark.parametrize("eager", [False, True], ids=["deltalog", "eager"])
+def test_deltanet_is_gdn_without_decay(eager):
+    """DeltaNet (the delta rule without a gate) is GDN with lambda = 0: the GDN
+    kernels, fed zero log-decays, follow the oracle on the full head shape through two
+    merges and a ragged partial cycle."""
+    M = 16
+    r = Rollout(W.GDN_B64, M=M, B=3, steps=2 * M + 5, eager=eager)
+    for t in range(r.steps):
+        x = dict(W.step_inputs(r.w, t, r.layer))
+        x["lam"] = np.zeros_like(x["lam"])
+        r._step_rows(x, np.arange(r.w.B))
+    _check(r, f"deltanet (gdn, lambda = 0) {'eager' if eager else 'deltalog'}")
