@@ -599,11 +599,11 @@ void deltalog_kernel(KParams p) {
 #pragma unroll
           for (int x = 0; x < RPL; ++x) {
             const int r = c_ * RPL + x;
-            ak = fmaf(kr[x], s_kf[r], ak);
+            if constexpr (CF::NEEDS_C) ak = fmaf(kr[x], s_kf[r], ak);
             aq = fmaf(kr[x], s_qf[r], aq);
           }
           const float w = CF::DECAY ? dl_exp(s_lr[0] - lr_[0]) : 1.f;
-          ak *= w;
+          if constexpr (CF::NEEDS_C) ak *= w;
           aq *= w;
           if (stage) {
 #pragma unroll
@@ -614,7 +614,7 @@ void deltalog_kernel(KParams p) {
           for (int x = 0; x < RPL; ++x) {
             const int r = c_ * RPL + x;
             const float wk = dl_exp(s_lr[r] - lr_[x]) * kr[x];
-            ak = fmaf(wk, s_kf[r], ak);
+            if constexpr (CF::NEEDS_C) ak = fmaf(wk, s_kf[r], ak);
             aq = fmaf(wk, s_qf[r], aq);
             if (stage) s_kt[r * CF::KTS + e_] = CF::BONUS ? dl_exp(s_lm[r] - lr_[x]) * kr[x] : wk;
           }
@@ -625,11 +625,11 @@ void deltalog_kernel(KParams p) {
       }
 #pragma unroll
       for (int m = CF::LPE / 2; m >= 1; m >>= 1) {
-        ak += shfl_xor(ak, m);
+        if constexpr (CF::NEEDS_C) ak += shfl_xor(ak, m);   // the delta-rule correction only
         aq += shfl_xor(aq, m);
       }
       if (c_ == 0 && i < L) {
-        s_gk[i] = ak;
+        if constexpr (CF::NEEDS_C) s_gk[i] = ak;
         s_gq[i] = aq;
       }
     }
