@@ -1,0 +1,73 @@
+"""Host-side parts of bench.py (no GPU): the one-GPU contract, the counter-profile
+lookup keyed by the kernel-source hash, the algorithmic bytes the roofline divides
+by, and the CPU-oracle baseline leg."""
+
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+
+import bench
+from paper_2608_15533_amd import traffic as T
+from paper_2608_15533_amd import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_more_than_one_gpu_is_refused_with_a_message():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+    assert r.stdout == ""
+
+
+def test_every_workload_has_a_positive_algorithmic_step():
+    for name, (w, R) in bench.workloads().items():
+        assert R >= 1, name
+        for L in range(w.M):
+            b = T.step_bytes(w.op, w.dk, w.dv, w.M, L, w.in_dtype).total
+            assert b > 0, (name, L)
+        # the dense state dominates every step: read always, written at the merge
+        state = w.dk * w.dv * 4
+        assert T.step_bytes(w.op, w.dk, w.dv, w.M, 0, w.in_dtype).total > state
+        assert T.step_bytes(w.op, w.dk, w.dv, w.M, w.M - 1, w.in_dtype).total > 2 * state
+
+
+def test_counter_traffic_follows_the_kernel_source_hash(monkeypatch, tmp_path):
+    key = "unit_test_workload"
+    prof = tmp_path / "profiles"
+    prof.mkdir()
+    (prof / f"{key}_hbm_counters.txt").write_text(
+        "# header\nTRAFFIC_JSON " + json.dumps({"kernel_source_hash": "abc",
+                                                 "step_kernel_bytes_per_launch": 123.0}) + "\n")
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    monkeypatch.setattr(bench, "kernel_source_hash", lambda: "abc")
+    val, src = bench.counter_traffic(key)
+    assert val == 123.0 and src.endswith(f"{key}_hbm_counters.txt")
+    monkeypatch.setattr(bench, "kernel_source_hash", lambda: "changed")
+    val, src = bench.counter_traffic(key)
+    assert val is None and "changed" in src
+    val, src = bench.counter_traffic("no_such_workload")
+    assert val is None and src == "no counter profile"
+
+
+def test_profile_keys():
+    assert bench.profile_key("gdn_b64_h32_d128_m16", "f32") == "gdn_b64_h32_d128_m16"
+    assert bench.profile_key("gdn_b64_h32_d128_m16", "bf16") == "gdn_b64_h32_d128_m16_bf16state"
+    assert bench.profile_key("x", "f32", tiled=2) == "x_tiled2_split"
+    assert bench.profile_key("x", "f32", tiled=4, fused_replay=True) == "x_tiled4_fused"
+
+
+def test_cpu_baseline_leg_reports_the_contract_fields():
+    res = bench.cpu_baseline(W.GDN_SMALL, 0.2)
+    assert res["kind"] == "oracle" and res["unit"] == "tokens/s"
+    assert res["value"] > 0 and res["cores"] >= 1
+    assert "fp64 eager oracle" in res["sample"]
+
+
+def test_kernel_source_hash_is_stable():
+    assert bench.kernel_source_hash() == bench.kernel_source_hash()
+    assert len(bench.kernel_source_hash()) == 16
