@@ -450,3 +450,48 @@ def test_embedded_2x2_bruteforce(op, M):
                                err_msg=f"{op} M={M} flushed block")
     Sg[:2, :2] = 0.0
     assert not np.any(Sg), f"{op} M={M}: state outside the block"
+
+
+@pytest.mark.parametrize("op", ["gdn", "rwkv6"])
+def test_independent_states_on_two_streams(op):
+    """The library keeps no state between calls: two layers stepped on two side streams
+    (default priority), their launches interleaved from one host thread, end bitwise
+    equal to the same layers stepped one after the other on the current stream."""
+    dl = D()
+    w = WL[op].with_(B=4)
+    M, steps = 4, 9
+    desc = dl.make_desc(op, w.B, w.H, w.dk, w.dv, M, w.in_dtype)
+    u = W.bonus(w)
+    S0 = [W.initial_state(w, layer) for layer in (0, 1)]
+    xs = [[W.step_inputs(w, t, layer) for t in range(steps)] for layer in (0, 1)]
+    toks = [[token(desc, x, u) for x in xs[layer]] for layer in (0, 1)]
+
+    def fresh():
+        return [dl.DeltaLogState(desc, to_dev(S0[layer], torch.float32)) for layer in (0, 1)]
+
+    def outs():
+        return [[torch.empty((w.B, w.H, w.dv), dtype=torch.float32, device="cuda")
+                 for _ in range(steps)] for _ in (0, 1)]
+
+    ref_st, ref_o = fresh(), outs()
+    for layer in (0, 1):
+        for t in range(steps):
+            dl.dl_append_step(desc, ref_st[layer], toks[layer][t], ref_o[layer][t])
+    torch.cuda.synchronize()
+
+    st, o = fresh(), outs()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    for s in streams:
+        s.wait_stream(torch.cuda.current_stream())
+    for t in range(steps):
+        for layer in (0, 1):
+            dl.dl_append_step(desc, st[layer], toks[layer][t], o[layer][t], stream=streams[layer])
+    for s in streams:
+        torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    for layer in (0, 1):
+        a, b = _state_arrays(ref_st[layer]), _state_arrays(st[layer])
+        for k in a:
+            np.testing.assert_array_equal(a[k], b[k], err_msg=(layer, k))
+        for t in range(steps):
+            assert torch.equal(ref_o[layer][t], o[layer][t]), (layer, t)
