@@ -119,16 +119,43 @@ def copy_calibration(mib):
                       "launches": 5}), flush=True)
 
 
+def code_only(text):
+    """C/C++ source text without comments and with every whitespace run collapsed to one
+    space (string and character literals kept verbatim): what the compiler sees, up to
+    layout."""
+    out, i, n = [], 0, len(text)
+    while i < n:
+        c = text[i]
+        if c in "\"'":
+            j = i + 1
+            while j < n and text[j] != c:
+                j += 2 if text[j] == "\\" else 1
+            out.append(text[i:j + 1])
+            i = j + 1
+        elif text.startswith("//", i):
+            j = text.find("\n", i)
+            i = n if j < 0 else j
+        elif text.startswith("/*", i):
+            j = text.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+            out.append(" ")
+        else:
+            out.append(c)
+            i += 1
+    return " ".join("".join(out).split())
+
+
 def kernel_source_hash():
-    """sha256 over the kernel sources and the public header (any change invalidates
-    counter figures taken earlier)."""
+    """sha256 over the code of the kernel sources and the public header, comments and
+    layout excluded: any change to the code invalidates counter figures taken earlier,
+    an edit of a comment does not."""
     files = sorted(glob.glob(os.path.join(ROOT, "paper_2608_15533_amd", "csrc", "*")))
     files.append(os.path.join(ROOT, "include", "deltalog.h"))
     h = hashlib.sha256()
     for f in files:
         h.update(os.path.basename(f).encode())
-        with open(f, "rb") as fh:
-            h.update(fh.read())
+        with open(f, encoding="utf-8", errors="surrogateescape") as fh:
+            h.update(code_only(fh.read()).encode("utf-8", errors="surrogateescape"))
     return h.hexdigest()[:16]
 
 

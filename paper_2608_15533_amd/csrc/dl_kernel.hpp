@@ -124,7 +124,7 @@ __device__ __forceinline__ float dl_exp(float x) { return __expf(x); }
 // head's base address lives in scalar registers, each lane keeps one 32-bit offset and
 // the row blocks differ by a scalar offset, so no per-row 64-bit addresses occupy
 // vector registers between the load and the store.  The resource covers exactly the
-// head's dk x dv floats; the hardware drops accesses outside it.
+// head's dk x dv state elements; the hardware drops accesses outside it.
 constexpr int kStateCachePolicy = DL_NT_STATE ? 2 : 0;   // 2 = non-temporal
 constexpr int kRawBufferFlags = 0x00020000;                // 32-bit data format, raw access
 
@@ -176,7 +176,8 @@ template <> struct StateQuad<uint16_t> {
   }
 };
 
-// N consecutive elements (N a multiple of 8) widened to fp32, loaded with 16-byte accesses.
+// N consecutive elements (N a multiple of 4) widened to fp32, loaded with 16-byte accesses
+// (8-byte accesses for bf16 runs whose length is not a multiple of 8).
 template <int N>
 __device__ __forceinline__ void ld_run(const float* p, float (&o)[N]) {
 #pragma unroll
@@ -232,7 +233,7 @@ template <> struct Raw4<uint16_t> {
   }
 };
 
-template <typename T, int N> struct RawRun;         // N consecutive elements, N % 8 == 0
+template <typename T, int N> struct RawRun;         // N consecutive elements, N % 4 == 0
 template <int N> struct RawRun<float, N> {
   float4 w[N / 4];
   __device__ __forceinline__ void load(const float* p) {

@@ -71,3 +71,25 @@ def test_cpu_baseline_leg_reports_the_contract_fields():
 def test_kernel_source_hash_is_stable():
     assert bench.kernel_source_hash() == bench.kernel_source_hash()
     assert len(bench.kernel_source_hash()) == 16
+
+
+def test_code_only_drops_comments_and_layout_but_keeps_literals():
+    src = ('int a = 1;   // trailing\n/* block\n comment */ const char* s = "// /* kept */";\n'
+           "char q = '\\'';\n#define X  2\n")
+    assert bench.code_only(src) == ('int a = 1; const char* s = "// /* kept */"; '
+                                    "char q = '\\''; #define X 2")
+
+
+def test_kernel_hash_ignores_comments_but_not_code(monkeypatch, tmp_path):
+    import shutil
+    shutil.copytree(os.path.join(ROOT, "paper_2608_15533_amd", "csrc"),
+                    tmp_path / "paper_2608_15533_amd" / "csrc")
+    shutil.copytree(os.path.join(ROOT, "include"), tmp_path / "include")
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    h0 = bench.kernel_source_hash()
+    f = tmp_path / "paper_2608_15533_amd" / "csrc" / "dl_kernel.hpp"
+    text = f.read_text()
+    f.write_text("// an added comment\n" + text.replace("\n\n", "\n\n\n", 1))
+    assert bench.kernel_source_hash() == h0
+    f.write_text(text.replace("#pragma once", "#pragma once\nstatic int dl_changed = 1;", 1))
+    assert bench.kernel_source_hash() != h0
