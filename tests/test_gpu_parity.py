@@ -140,3 +140,50 @@ def test_deltanet_is_gdn_without_decay(eager):
         x["lam"] = np.zeros_like(x["lam"])
         r._step_rows(x, np.arange(r.w.B))
     _check(r, f"deltanet (gdn, lambda = 0) {'eager' if eager else 'deltalog'}")
+
+
+CAMPAIGN = [("gdn", W.GDN_B64, 16), ("kda", W.KDA_B128, 16), ("rwkv6", W.RWKV6_B128, 16)]
+
+
+@pytest.mark.parametrize("B", [64, 128, 256])
+@pytest.mark.parametrize("op,w,M", CAMPAIGN, ids=[o for o, _, _ in CAMPAIGN])
+def test_rollout_against_dense_eager_all_slots(op, w, M, B):
+    """The numerical check of Sec. 5 at full size: 128-token rollouts at B in {64, 128,
+    256}, DeltaLog against the eager dense kernel on the same inputs, every slot and
+    head compared.  Reports the largest output relative error (over steps, and over
+    single (slot, head) rows) and the state relative error after a flush; both paths
+    are fp32, so the bar is the fp32 one."""
+    import torch
+    from gpu_harness import D, to_dev, token
+
+    dl = D()
+    w = w.with_(B=B)
+    steps = 128
+    desc = dl.make_desc(op, B, w.H, w.dk, w.dv, M, w.in_dtype)
+    S0 = W.initial_state(w)
+    st = dl.DeltaLogState(desc, to_dev(S0, torch.float32))
+    Se = to_dev(S0, torch.float32)
+    del S0
+    u = W.bonus(w)
+    o = torch.empty((B, w.H, w.dv), dtype=torch.float32, device="cuda")
+    oe = torch.empty_like(o)
+    worst_step = worst_row = 0.0
+    for t in range(steps):
+        tok = token(desc, W.step_inputs(w, t), u)
+        dl.dl_append_step(desc, st, tok, o)
+        dl.dl_eager_step(desc, Se, tok, oe)
+        diff = (o - oe).double()
+        ref = oe.double()
+        worst_step = max(worst_step, float(diff.norm() / ref.norm()))
+        row = diff.norm(dim=-1) / ref.norm(dim=-1).clamp_min(1e-30)
+        worst_row = max(worst_row, float(row.max()))
+    dl.dl_merge(desc, st)
+    torch.cuda.synchronize()
+    ds = (st.S.double() - Se.double())
+    state_err = float(ds.norm() / Se.double().norm())
+    state_row = float((ds.flatten(2).norm(dim=-1) / Se.double().flatten(2).norm(dim=-1)).max())
+    log(f"{op} B={B} M={M}, 128 steps vs eager: output rel err max over steps {worst_step:.2e}, "
+        f"max over (step, slot, head) {worst_row:.2e}; flushed state rel err {state_err:.2e}, "
+        f"max over (slot, head) {state_row:.2e}")
+    assert int(st.err.item()) == 0
+    assert worst_row <= TOL_F32_STATE and state_row <= TOL_F32_STATE
