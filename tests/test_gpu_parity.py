@@ -187,3 +187,37 @@ def test_rollout_against_dense_eager_all_slots(op, w, M, B):
         f"max over (slot, head) {state_row:.2e}")
     assert int(st.err.item()) == 0
     assert worst_row <= TOL_F32_STATE and state_row <= TOL_F32_STATE
+
+
+# beta exists only for the delta rule; linear attention has no decay to vary
+DEGENERATE = [(op, case) for op in ("gdn", "kda", "rwkv6", "linattn", "retnet", "gla")
+              for case in ("zero_beta", "zero_keys", "strong_decay", "no_decay")
+              if not (case == "zero_beta" and op not in ("gdn", "kda"))
+              and not (case in ("strong_decay", "no_decay") and op == "linattn")]
+
+
+@pytest.mark.parametrize("op,case", DEGENERATE, ids=[f"{o}-{c}" for o, c in DEGENERATE])
+def test_degenerate_inputs(op, case):
+    """Degenerate gates and factors through two merge cycles at full head shape: no write
+    (beta = 0, delta rule only), zero keys (no update at all), a decay so strong that
+    exp(ell) underflows within the cycle (lambda = -30 per step; every factor is an exp
+    of a log-decay difference, so nothing overflows), and no decay (lambda = 0).  The
+    oracle follows every slot; the bar is the fp32 one and no NaN or Inf may appear."""
+    w = {"gdn": W.GDN_B64, "kda": W.KDA_B128, "rwkv6": W.RWKV6_B128,
+         "linattn": W.LINATTN_B64, "retnet": W.RETNET_B64, "gla": W.GLA_B128}[op]
+    M = 8
+    r = Rollout(w, M=M, B=2, steps=2 * M + 3)
+    for t in range(r.steps):
+        x = dict(W.step_inputs(r.w, t, r.layer))
+        if case == "zero_beta":
+            x["beta"] = np.zeros_like(x["beta"])
+        elif case == "zero_keys":
+            x["k"] = np.zeros_like(x["k"])
+        elif case == "strong_decay":
+            x["lam"] = np.full_like(x["lam"], -30.0)
+        else:
+            x["lam"] = np.zeros_like(x["lam"])
+        r._step_rows(x, np.arange(r.w.B))
+    o = r.o.cpu().numpy()
+    assert np.isfinite(o).all() and np.isfinite(r.base().float().cpu().numpy()).all()
+    _check(r, f"{op} {case}")
