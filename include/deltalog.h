@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define DL_ABI_VERSION 3
+#define DL_ABI_VERSION 4
 #define DL_MAX_MERGE_INTERVAL 64
 
 typedef enum {
@@ -90,7 +90,10 @@ typedef enum { DL_F32 = 0, DL_BF16 = 1 } dl_dtype;
  *   RETNET  head-wise scalar decay gamma_t = exp(lambda_t), pair (k, v), o = q^T S_t;
  *   GLA     per-key decay, pair (k, v), o = q^T S_t.
  * dl (the log-decay width) is dk for KDA, RWKV6 and GLA and 1 for GDN and RetNet;
- * linear attention has no log-decay and touches none of ell, lam_log or lam. */
+ * linear attention has no log-decay and touches none of ell, lam_log or lam.
+ * The cumulative log-decay ell is stored for per-key decay only: with one log-decay per
+ * head it always equals the newest snapshot Lam_log[L-1] (Eq. 5 writes both with the
+ * same value; 0 when L = 0), and the library reads it from there. */
 typedef struct {
   int32_t abi_version;    /* must be DL_ABI_VERSION                                      */
   int32_t op;             /* dl_op                                                       */
@@ -109,8 +112,9 @@ typedef struct {
 /* DeltaLog physical state (Sec. 3.1 list of buffers), one entry per (slot, head). */
 typedef struct {
   void*    S;        /* [B,H,dk,dv] state_dtype dense base                               */
-  float*   ell;      /* [B,H,dl]    fp32 cumulative log-decay since the last merge       */
-                     /*             (ignored, may be NULL, for LINATTN)                  */
+  float*   ell;      /* [B,H,dk]    fp32 cumulative log-decay since the last merge, for  */
+                     /*             KDA, RWKV6, GLA; ignored (may be NULL) for GDN,      */
+                     /*             RetNet (see dl_desc) and LINATTN                     */
   void*    k_log;    /* [B,H,C,dk]  in_dtype   key-side factors   (may be NULL if C == 0) */
   void*    u_log;    /* [B,H,C,dv]  u_log_dtype value-side factors (may be NULL if C == 0)*/
   float*   lam_log;  /* [B,H,C,dl]  fp32 snapshot of ell per entry (may be NULL if C == 0)*/
@@ -170,7 +174,7 @@ int dl_readout(const dl_desc* desc, const dl_state* state, const void* q, float*
  *                 the prepared coefficients, or recomputing them per tile when
  *                 split_replay == 0), write the output slice, append the tile's U_log
  *                 shard (tile 0 also writes K_log[L] and Lam_log[L]) or merge the tile;
- *   Finalize      per (row, head): commit ell and L exactly once.
+ *   Finalize      per (row, head): commit L (and ell, where stored) exactly once.
  * value_tiles: 2 or 4.  Only state_dtype == DL_F32 (else DL_E_DTYPE).
  * workspace: device memory of at least dl_tiled_workspace_bytes(desc, n) bytes, 16-byte
  * aligned, owned by the caller; required when split_replay != 0 and C > 0, ignored

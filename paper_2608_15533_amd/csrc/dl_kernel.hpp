@@ -290,6 +290,15 @@ __device__ __forceinline__ size_t lam_log_stride(const KParams& p) {
   return DL == 1 ? size_t(p.H) : size_t(DL);
 }
 
+// Read one float at a workgroup-uniform address through the scalar path (the constant
+// address space): the read waits on its own counter instead of queueing behind the
+// vector loads in flight.  Only for data that no workgroup of the launch writes (the
+// scalar cache is invalidated at every kernel launch).
+__device__ __forceinline__ float scalar_ld(const float* ptr) {
+  typedef const float __attribute__((address_space(4))) const_float;
+  return *(const_float*)ptr;
+}
+
 // Nothing may be scheduled across this point (loads keep their issue order).
 __device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
 
@@ -312,6 +321,9 @@ struct OpTraits {
   static constexpr bool PER_KEY = OP == OP_KDA || OP == OP_RWKV6 || OP == OP_GLA;
   static constexpr bool DECAY = OP != OP_LINATTN;               // linear attention: none
   static constexpr bool BONUS = OP == OP_RWKV6;   // pre-update readout plus r^T diag(u) k v^T
+  // A stored cumulative log-decay (ell): per-key decay only.  For one log-decay per head
+  // it is the newest Lam_log snapshot (0 with an empty log) and is read from there.
+  static constexpr bool KEEPS_ELL = PER_KEY;
 };
 
 template <int OP, int DK, int DV, int MODE>
@@ -330,6 +342,7 @@ struct Cfg {
   static constexpr bool DELTA = OpTraits<OP>::DELTA;
   static constexpr bool DECAY = OpTraits<OP>::DECAY;
   static constexpr bool BONUS = OpTraits<OP>::BONUS;
+  static constexpr bool KEEPS_ELL = OpTraits<OP>::KEEPS_ELL;
   static constexpr bool HAS_LOG = MODE != M_EAGER;
   static constexpr bool HAS_TOKEN = MODE == M_EAGER || MODE == M_STEP || MODE == M_MERGE;
   static constexpr bool READS_OUT = MODE != M_FLUSH;
@@ -393,7 +406,7 @@ void deltalog_kernel(KParams p) {
   const int H = p.H;
   // Workgroups are dispatched round-robin over the 8 XCDs (each with its own L2).  Map
   // them so that each XCD owns whole chunks of DL_XCD_CHUNK consecutive (row, head)
-  // pairs: the 4-byte per-head metadata (ell, L, scalar log-decay snapshots) and token
+  // pairs: the 4-byte per-head metadata (L and the head-wise log-decay snapshots) and token
   // scalars of a chunk then fill whole 128-byte lines in one L2 instead of being
   // written back partially by eight different caches.  Chunks are dealt to the XCDs
   // in turn, so a run of consecutive slots that merge in the same step (slots admitted
@@ -449,7 +462,7 @@ void deltalog_kernel(KParams p) {
     if constexpr (CF::BONUS) uf = p.u[size_t(h) * DK + rl];
   }
   if constexpr (CF::READS_OUT) q_raw = qin[rl];
-  if constexpr (CF::HAS_LOG && CF::DECAY) ell = p.ell[sh * DL + rd];
+  if constexpr (CF::HAS_LOG && CF::KEEPS_ELL) ell = p.ell[sh * DL + rd];
   Raw4<TIN> v_raw{};
   float beta = 0.f;
   if constexpr (CF::HAS_TOKEN) {
@@ -489,6 +502,12 @@ void deltalog_kernel(KParams p) {
   const float* Lb = Lw;
   const size_t LS = lam_log_stride<DL>(p);
   const TU* Ub = static_cast<const TU*>(p.u_log) + sh * size_t(C) * DV;
+  // Head-wise decay keeps no separate cumulative log-decay: after an append it equals
+  // the newest snapshot (Eq. 5 writes both with the same value), after a merge it is 0.
+  // Entry L-1 is not written by this launch (the append writes entry L), so it is read
+  // through the scalar path, without waiting for the tile in flight.
+  if constexpr (CF::HAS_LOG && CF::DECAY && !CF::KEEPS_ELL)
+    ell = L > 0 ? scalar_ld(Lb + size_t(L - 1) * LS) : 0.f;
   const int e_ = tid / CF::LPE;                   // coefficient pass: entry within the pass
   const int c_ = tid % CF::LPE;                   //                   key-row run
   // Per-key snapshots are prefetched only where the registers allow it (small heads).
@@ -732,7 +751,7 @@ void deltalog_kernel(KParams p) {
       if constexpr (CF::DECAY) {
         for (int x = tid; x < DL; x += NT) {
           Lw[size_t(L) * LS + x] = s_lm[x];
-          p.ell[sh * DL + x] = s_lm[x];
+          if constexpr (CF::KEEPS_ELL) p.ell[sh * DL + x] = s_lm[x];
         }
       }
       if (tid == 0) p.len[sh] = L + 1;
@@ -794,7 +813,7 @@ void deltalog_kernel(KParams p) {
 #pragma unroll
     for (int j = 0; j < RPT; ++j) StateQuad<TS>::store(srs, toff, j * kRowBlock, m[j]);
     if constexpr (CF::HAS_LOG) {
-      if constexpr (CF::DECAY)
+      if constexpr (CF::KEEPS_ELL)
         for (int x = tid; x < DL; x += NT) p.ell[sh * DL + x] = 0.f;
       if (tid == 0) p.len[sh] = 0;
     }

@@ -82,6 +82,22 @@ __device__ __forceinline__ void replay_coefficients(const TIN* Kb, const float* 
   }
 }
 
+// Cumulative log-decay of a (slot, head) at live length L, element x: stored for
+// per-key decay; for one log-decay per head, the newest snapshot (0 with an empty log).
+template <int OP, int DK>
+__device__ __forceinline__ float cumulative_decay(const KParams& p, size_t sh, int L, int x) {
+  using TR = OpTraits<OP>;
+  if constexpr (!TR::DECAY) {
+    return 0.f;
+  } else if constexpr (TR::KEEPS_ELL) {
+    return p.ell[sh * DK + x];
+  } else {
+    const int slot = int(sh / size_t(p.H)), h = int(sh % size_t(p.H));
+    return L > 0 ? scalar_ld(lam_log_base<1>(p, slot, h) + size_t(L - 1) * lam_log_stride<1>(p))
+                 : 0.f;
+  }
+}
+
 // Live length of a (slot, head) if the row's slot and the length are valid, else -1.
 __device__ __forceinline__ int tiled_row(const KParams& p, int row, int h, size_t& sh) {
   const int slot = p.slots ? p.slots[row] : row;
@@ -110,7 +126,7 @@ __global__ __launch_bounds__(256) void replay_prep_kernel(KParams p, float* coef
   if (tid < DL) {
     float lr = 0.f;
     if constexpr (TR::DECAY) {
-      const float ell = p.ell[sh * DL + tid];
+      const float ell = cumulative_decay<OP, DK>(p, sh, L, tid);
       lr = TR::BONUS ? ell : ell + p.lam[th * DL + tid];   // readout decay, as in the step
     }
     s_lr[tid] = lr;
@@ -200,7 +216,7 @@ void tile_step_kernel(KParams p, const float* __restrict__ coef) {
     if constexpr (TR::BONUS) uf = p.u[size_t(h) * DK + tid];
     float ell = 0.f, lam = 0.f;
     if constexpr (TR::DECAY) {
-      ell = p.ell[sh * DL + (DL == 1 ? 0 : tid)];
+      ell = cumulative_decay<OP, DK>(p, sh, L, DL == 1 ? 0 : tid);
       lam = p.lam[th * DL + (DL == 1 ? 0 : tid)];
     }
     const float lm = ell + lam;
@@ -361,7 +377,8 @@ void tile_step_kernel(KParams p, const float* __restrict__ coef) {
 
 // ------------------------------------------------------------------ Finalize
 // One wave per (row, head): append -> ell += lambda, L + 1; merge -> ell = 0, L = 0.
-// ell + lambda is the same fp32 sum the tiles used for Lam_log[L].
+// ell + lambda is the same fp32 sum the tiles used for Lam_log[L].  Head-wise decay
+// stores no ell (it is read back from Lam_log), so only L is committed there.
 template <int OP, int DK>
 __global__ __launch_bounds__(64) void finalize_kernel(KParams p) {
   using TR = OpTraits<OP>;
@@ -373,11 +390,11 @@ __global__ __launch_bounds__(64) void finalize_kernel(KParams p) {
   if (L < 0) return;                                // invalid: reported by the tiles
   const size_t th = size_t(row) * p.H + h;
   if (L < p.C) {
-    if constexpr (TR::DECAY)
+    if constexpr (TR::KEEPS_ELL)
       for (int x = tid; x < DL; x += 64) p.ell[sh * DL + x] = p.ell[sh * DL + x] + p.lam[th * DL + x];
     if (tid == 0) p.len[sh] = L + 1;
   } else {
-    if constexpr (TR::DECAY)
+    if constexpr (TR::KEEPS_ELL)
       for (int x = tid; x < DL; x += 64) p.ell[sh * DL + x] = 0.f;
     if (tid == 0) p.len[sh] = 0;
   }

@@ -27,7 +27,7 @@ if not os.path.exists(LIB_PATH):
 _lib = ctypes.CDLL(LIB_PATH)
 
 # ----------------------------------------------------------------- constants (deltalog.h)
-DL_ABI_VERSION = 3
+DL_ABI_VERSION = 4
 DL_MAX_MERGE_INTERVAL = 64
 DL_OK, DL_E_NULL, DL_E_SHAPE, DL_E_DTYPE, DL_E_ALIGN, DL_E_UNSUPPORTED, DL_E_HIP, DL_E_VERSION = (
     0, -1, -2, -3, -4, -5, -6, -7)
@@ -145,11 +145,13 @@ def _need(t, name, dtype, shape, device=None):
 class DeltaLogState:
     """Device buffers of the physical state (Sec. 3.1), allocated with torch.
 
-    S [B,H,dk,dv] state dtype, ell [B,H,dl] f32, k_log [B,H,C,dk] in_dtype,
-    u_log [B,H,C,dv], lam_log [B,H,C,dl] f32, len [B,H] int32, err [1] int32.  ``S``
-    starts as a copy of ``S0`` (the prefill state, converted to the state dtype); the
-    log starts empty (Sec. 4 slot lifecycle).  Linear attention has no decay: ``ell``
-    and ``lam_log`` are None and passed to the library as NULL.
+    S [B,H,dk,dv] state dtype, ell [B,H,dk] f32 (per-key decay only), k_log [B,H,C,dk]
+    in_dtype, u_log [B,H,C,dv], lam_log [B,H,C,dl] f32 ([B,C,H] for one log-decay per
+    head), len [B,H] int32, err [1] int32.  ``S`` starts as a copy of ``S0`` (the
+    prefill state, converted to the state dtype); the log starts empty (Sec. 4 slot
+    lifecycle).  With one log-decay per head (GDN, RetNet) the cumulative log-decay is
+    the newest snapshot and ``ell`` is None; linear attention has no decay, so ``ell``
+    and ``lam_log`` are None.  None buffers are passed to the library as NULL.
     """
 
     def __init__(self, desc, S0=None, device="cuda"):
@@ -163,7 +165,9 @@ class DeltaLogState:
         st = state_torch_dtype(desc)
         self.S = (torch.zeros((B, H, dk, dv), dtype=st, device=device) if S0 is None else
                   S0.to(device=device, dtype=st).contiguous().clone())
-        self.ell = torch.zeros((B, H, dl), **f32) if dl else None
+        # the cumulative log-decay is stored for per-key decay only; with one log-decay
+        # per head the library reads it from the newest Lam_log snapshot
+        self.ell = torch.zeros((B, H, dl), **f32) if dl > 1 else None
         self.k_log = torch.zeros((B, H, max(C, 0), dk), dtype=in_t, device=device)
         self.u_log = torch.zeros((B, H, max(C, 0), dv), dtype=u_t, device=device)
         # scalar snapshots are entry-major [B, C, H] (the heads of a slot side by side)

@@ -15,7 +15,11 @@ phase, with the precisions the library uses:
   activation dtype and U_log fp32 for the delta rule (GDN/KDA: computed values), the
   activation dtype for the others (exact copies of v).
 * cumulative log-decay ``C_decay``: 4 d_lambda bytes, read and written every DeltaLog step
-  (d_lambda = 0 for linear attention: no decay, no snapshots).
+  in the paper's representation (d_lambda = 0 for linear attention: no decay, no
+  snapshots).  This library stores it for per-key decay only: with one log-decay per
+  head it equals the newest snapshot, which the replay reads anyway, so the step moves
+  no separate ``C_decay`` bytes (``stored_ell=None`` selects the library's layout,
+  ``True`` the paper's).
 * the output o: fp32, dv values.
 * live-length and index metadata are omitted as lower-order, as the paper does.
 
@@ -26,6 +30,8 @@ Per phase (one head, one token):
                  write C_entry + C_decay + o
     merge at L   read  T_common + C_state + C_decay + L C_entry
                  write C_state + C_decay + o
+
+(C_decay counted only where the cumulative log-decay is stored.)
 """
 
 from dataclasses import dataclass
@@ -64,48 +70,73 @@ def eager_bytes(op, dk, dv, in_dtype="bf16", state_dtype="f32"):
     return HeadTraffic(read=common + state, write=state + out)
 
 
-def append_bytes(op, dk, dv, L, in_dtype="bf16", state_dtype="f32"):
+def stores_ell(op):
+    """Whether this library keeps a cumulative log-decay buffer for ``op`` (per-key decay
+    only; with one log-decay per head it is the newest snapshot)."""
+    return op in PER_KEY_OPS
+
+
+def _ell(op, decay, stored_ell):
+    return decay if (stores_ell(op) if stored_ell is None else stored_ell) else 0
+
+
+def append_bytes(op, dk, dv, L, in_dtype="bf16", state_dtype="f32", stored_ell=None):
     """Bytes of a DeltaLog append step taken at live length L."""
     common, state, entry, decay, out = _sizes(op, dk, dv, in_dtype, state_dtype)
-    return HeadTraffic(read=common + state + decay + L * entry, write=entry + decay + out)
+    ell = _ell(op, decay, stored_ell)
+    return HeadTraffic(read=common + state + ell + L * entry, write=entry + ell + out)
 
 
-def merge_bytes(op, dk, dv, L, in_dtype="bf16", state_dtype="f32"):
+def merge_bytes(op, dk, dv, L, in_dtype="bf16", state_dtype="f32", stored_ell=None):
     """Bytes of a DeltaLog merge step that folds L live entries (plus the token)."""
     common, state, entry, decay, out = _sizes(op, dk, dv, in_dtype, state_dtype)
-    return HeadTraffic(read=common + state + decay + L * entry, write=state + decay + out)
+    ell = _ell(op, decay, stored_ell)
+    return HeadTraffic(read=common + state + ell + L * entry, write=state + ell + out)
 
 
-def step_bytes(op, dk, dv, M, L, in_dtype="bf16", state_dtype="f32"):
+def step_bytes(op, dk, dv, M, L, in_dtype="bf16", state_dtype="f32", stored_ell=None):
     """Bytes of the Alg. 1 step at live length L: append if L < M-1, else merge."""
     if L < M - 1:
-        return append_bytes(op, dk, dv, L, in_dtype, state_dtype)
-    return merge_bytes(op, dk, dv, L, in_dtype, state_dtype)
+        return append_bytes(op, dk, dv, L, in_dtype, state_dtype, stored_ell)
+    return merge_bytes(op, dk, dv, L, in_dtype, state_dtype, stored_ell)
 
 
-def cycle_bytes(op, dk, dv, M, in_dtype="bf16", state_dtype="f32"):
+def cycle_bytes(op, dk, dv, M, in_dtype="bf16", state_dtype="f32", stored_ell=None):
     """Total bytes of one full cycle (M-1 appends at L = 0..M-2, one merge at L = M-1)."""
     r = w = 0
     for L in range(M):
-        t = step_bytes(op, dk, dv, M, L, in_dtype, state_dtype)
+        t = step_bytes(op, dk, dv, M, L, in_dtype, state_dtype, stored_ell)
         r += t.read
         w += t.write
     return HeadTraffic(read=r, write=w)
 
 
-def amortized_bytes_per_token(op, dk, dv, M, in_dtype="bf16", state_dtype="f32"):
+def amortized_bytes_per_token(op, dk, dv, M, in_dtype="bf16", state_dtype="f32",
+                              stored_ell=None):
     """Average bytes per head-token over a cycle (the Eq. 10 quantity, plus outputs)."""
-    c = cycle_bytes(op, dk, dv, M, in_dtype, state_dtype)
+    c = cycle_bytes(op, dk, dv, M, in_dtype, state_dtype, stored_ell)
     return c.total / M
 
 
-def state_write_ratio(op, dk, dv, M, in_dtype="bf16", state_dtype="f32", live_length_bytes=0):
-    """Eager / DeltaLog state-write bytes per token, outputs excluded: M / (1 + eps).
-    ``live_length_bytes`` adds the per-step write of the live length (metadata the model
-    of Eq. 9 omits; 4 for the int32 length this library keeps per slot and head)."""
+def state_write_ratio(op, dk, dv, M, in_dtype="bf16", state_dtype="f32", live_length_bytes=0,
+                      stored_ell=True):
+    """Eager / DeltaLog state-write bytes per token, outputs excluded.  With the defaults
+    this is the bound of Eq. 9, M / (1 + eps), in the paper's representation (the
+    cumulative log-decay written every step).  ``live_length_bytes`` adds the per-step
+    write of the live length (metadata the paper's model omits; 4 for the int32 length
+    this library keeps per slot and head); ``stored_ell=None`` counts the cumulative
+    log-decay only where this library stores it."""
     _, state, entry, decay, _ = _sizes(op, dk, dv, in_dtype, state_dtype)
-    dl_writes = (state + (M - 1) * entry + M * (decay + live_length_bytes)) / M
+    ell = _ell(op, decay, stored_ell)
+    dl_writes = (state + (M - 1) * entry + M * (ell + live_length_bytes)) / M
     return state / dl_writes
+
+
+def library_state_write_ratio(op, dk, dv, M, in_dtype="bf16", state_dtype="f32"):
+    """The write ratio this library's layout implies: the log entries, the cumulative
+    log-decay where it is stored, and the 4-byte live length of every head-step."""
+    return state_write_ratio(op, dk, dv, M, in_dtype, state_dtype, live_length_bytes=4,
+                             stored_ell=None)
 
 
 def byte_optimal_merge_interval(op, dk, dv, in_dtype="bf16", state_dtype="f32", max_M=64):

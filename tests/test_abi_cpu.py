@@ -36,7 +36,7 @@ def test_header_functions_are_exported():
 
 
 def test_version_and_status_strings():
-    assert D.dl_abi_version() == D.DL_ABI_VERSION == 3
+    assert D.dl_abi_version() == D.DL_ABI_VERSION == 4
     for code in range(0, -8, -1):
         s = D.dl_status_str(code)
         assert s.startswith("DL_") and s != "unknown dl_status"
@@ -121,9 +121,29 @@ def test_slot_list_rules():
     assert append(desc(), slots=A + 2, n=3) == D.DL_E_ALIGN
 
 
-@pytest.mark.parametrize("field", ["S", "ell", "len", "k_log", "u_log", "lam_log"])
+@pytest.mark.parametrize("field", ["S", "len", "k_log", "u_log", "lam_log"])
 def test_state_nulls(field):
     assert append(desc(), s=state(**{field: None})) == D.DL_E_NULL
+
+
+@pytest.mark.parametrize("op", ["kda", "rwkv6", "gla"])
+def test_per_key_decay_needs_the_cumulative_log_decay(op):
+    d = D.make_desc(op, 4, 2, 128, 128, 16, "bf16")
+    t = token(beta=None) if op != "kda" else token()
+    if op == "rwkv6":
+        t = token(beta=None, u=A + 0xC00000)
+    assert append(d, s=state(ell=None), t=t) == D.DL_E_NULL
+    assert append(d, s=state(ell=A + 0x100002), t=t) == D.DL_E_ALIGN
+
+
+@pytest.mark.parametrize("op", ["gdn", "retnet"])
+def test_head_wise_decay_ignores_the_cumulative_log_decay(op):
+    """One log-decay per head: ell is read back from the newest snapshot, so a NULL or
+    misaligned ell passes the checks (the call then stops at the misaligned output)."""
+    d = D.make_desc(op, 4, 2, 128, 128, 16, "bf16")
+    t = token() if op == "gdn" else token(beta=None)
+    assert append(d, s=state(ell=None), t=t, o=A + 4) == D.DL_E_ALIGN
+    assert append(d, s=state(ell=A + 0x100002), t=t, o=A + 4) == D.DL_E_ALIGN
 
 
 def test_log_buffers_optional_when_M_is_1():
@@ -158,7 +178,8 @@ def test_decaying_additive_operators_need_lam_not_beta(op):
     d = D.make_desc(op, 4, 2, 128, 128, 16, "bf16")
     assert append(d, t=token(beta=None), o=A + 4) == D.DL_E_ALIGN
     assert append(d, t=token(lam=None, beta=None)) == D.DL_E_NULL
-    assert append(d, s=state(ell=None), t=token(beta=None)) == D.DL_E_NULL
+    if op == "gla":
+        assert append(d, s=state(ell=None), t=token(beta=None)) == D.DL_E_NULL
     assert append(d, s=state(lam_log=None), t=token(beta=None)) == D.DL_E_NULL
 
 
@@ -172,7 +193,7 @@ def test_additive_u_log_holds_copies_of_v(op):
 
 
 @pytest.mark.parametrize("where,field,off", [
-    ("state", "S", 8), ("state", "k_log", 4), ("state", "u_log", 8), ("state", "ell", 2),
+    ("state", "S", 8), ("state", "k_log", 4), ("state", "u_log", 8), ("state", "lam_log", 2),
     ("token", "q", 8), ("token", "k", 2), ("token", "v", 4), ("token", "lam", 1),
 ])
 def test_alignment(where, field, off):

@@ -45,7 +45,7 @@ def _call(entry, d, s, t, n, slots, extra):
 
 
 DESC_FIELDS = {
-    "abi_version": [1, 2, 3, 4],
+    "abi_version": [1, 3, 4, 5],
     "op": [-1, 0, 1, 2, 3, 4, 5, 6],
     "num_slots": [-1, 0, 1, 4],
     "heads": [-1, 0, 1, 2],
@@ -92,7 +92,7 @@ def test_valid_call_stops_at_the_output_alignment(entry):
 
 
 @pytest.mark.parametrize("field,value,code", [
-    ("abi_version", 4, D.DL_E_VERSION), ("op", 6, D.DL_E_UNSUPPORTED),
+    ("abi_version", 5, D.DL_E_VERSION), ("op", 6, D.DL_E_UNSUPPORTED),
     ("dk", 96, D.DL_E_UNSUPPORTED), ("merge_interval", 65, D.DL_E_UNSUPPORTED),
     ("num_slots", 0, D.DL_E_SHAPE), ("in_dtype", 2, D.DL_E_DTYPE),
     ("state_dtype", 3, D.DL_E_DTYPE),

@@ -192,7 +192,8 @@ def test_batch_composition_invariance(op):
 @pytest.mark.parametrize("op", OPS)
 def test_log_contents_match_the_model(op):
     """After L appends the log holds: K_log = k bitwise (exact copies), Lam_log and ell =
-    the cumulative log-decay (none for linear attention), U_log = the delta-rule values b
+    the cumulative log-decay (ell stored for per-key decay, the newest Lam_log entry for
+    head-wise decay, none for linear attention), U_log = the delta-rule values b
     (GDN/KDA) or v bitwise (the others), len = L -- compared with the fp64 Alg. 1 model."""
     w = WL[op].with_(B=3)
     M, steps = 8, 5
@@ -218,8 +219,13 @@ def test_log_contents_match_the_model(op):
         lam_log = a["lam_log"]
         if lam_log.ndim == 3:               # scalar snapshots: entry-major [B, C, H]
             lam_log = lam_log.transpose(0, 2, 1)[..., None]
-        assert rel(lam_log.reshape(N, M - 1, -1)[:, :L], model.Lam[:, :L]) <= 1e-6
-        assert rel(a["ell"].reshape(N, -1), model.ell) <= 1e-6
+        lam_log = lam_log.reshape(N, M - 1, -1)
+        assert rel(lam_log[:, :L], model.Lam[:, :L]) <= 1e-6
+        if "ell" in a:                      # stored for per-key decay
+            assert rel(a["ell"].reshape(N, -1), model.ell) <= 1e-6
+        else:                               # one log-decay per head: the newest snapshot
+            assert op in ("gdn", "retnet")
+            assert rel(lam_log[:, L - 1], model.ell) <= 1e-6
     U = a["u_log"].astype(np.float64).reshape(N, M - 1, w.dv)[:, :L]
     if op not in OE.DELTA_OPS:
         np.testing.assert_array_equal(U, model.U[:, :L])

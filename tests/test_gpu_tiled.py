@@ -126,7 +126,8 @@ def test_tiled_bad_slot_sets_error_word_and_writes_nothing():
     desc = dl.make_desc("gdn", w.B, w.H, w.dk, w.dv, 4, w.in_dtype)
     st = dl.DeltaLogState(desc, to_dev(W.initial_state(w), torch.float32))
     ws = dl.tiled_workspace(desc, 1)
-    before = {k: v.float().cpu().numpy().copy() for k, v in st.buffers().items()}
+    before = {k: v.float().cpu().numpy().copy() for k, v in st.buffers().items()
+              if v is not None}
     x = W.step_inputs(w, 0)
     o = torch.zeros((1, w.H, w.dv), dtype=torch.float32, device="cuda")
     dl.dl_append_step_tiled(desc, st, token(desc, x, rows=[0]), o,
@@ -135,5 +136,5 @@ def test_tiled_bad_slot_sets_error_word_and_writes_nothing():
     torch.cuda.synchronize()
     assert int(st.err.item()) == 1
     for k, v in st.buffers().items():
-        if k != "err":
+        if k != "err" and v is not None:
             np.testing.assert_array_equal(before[k], v.float().cpu().numpy(), err_msg=k)

@@ -23,11 +23,11 @@ def test_read_traffic_reproduces_printed_counters():
     g = _gold()
     heads = g["B"] * g["H"]
     args = (g["op"], g["dk"], g["dv"])
-    pts = {
+    pts = {                                  # the paper's representation (ell stored)
         "dense_read": T.eager_bytes(*args).read,
-        "append_read_L0": T.append_bytes(*args, 0).read,
-        "append_read_L6": T.append_bytes(*args, 6).read,
-        "merge_read_L7": T.merge_bytes(*args, 7).read,
+        "append_read_L0": T.append_bytes(*args, 0, stored_ell=True).read,
+        "append_read_L6": T.append_bytes(*args, 6, stored_ell=True).read,
+        "merge_read_L7": T.merge_bytes(*args, 7, stored_ell=True).read,
     }
     for key, per_head in pts.items():
         model = per_head * heads / GIB
@@ -51,18 +51,29 @@ def test_write_ratio_bounds_printed_reduction():
     ("rwkv6", 64, 16, "bf16", 33664, 18304, 41856),
 ])
 def test_per_head_bytes(op, dk, M, in_dtype, eager, app0, merge):
-    """Hand-summed per-head totals (fp32 output, fp32 state) for the tested shapes."""
+    """Hand-summed per-head totals (fp32 output, fp32 state) for the tested shapes, in
+    the paper's representation; this library's layout drops the 4-byte cumulative
+    log-decay read and write of head-wise decay (8 bytes per step) and matches it for
+    per-key decay."""
     assert T.eager_bytes(op, dk, dk, in_dtype).total == eager
-    assert T.append_bytes(op, dk, dk, 0, in_dtype).total == app0
-    assert T.merge_bytes(op, dk, dk, M - 1, in_dtype).total == merge
+    assert T.append_bytes(op, dk, dk, 0, in_dtype, stored_ell=True).total == app0
+    assert T.merge_bytes(op, dk, dk, M - 1, in_dtype, stored_ell=True).total == merge
+    saved = 0 if T.stores_ell(op) else 8
+    assert T.append_bytes(op, dk, dk, 0, in_dtype).total == app0 - saved
+    assert T.merge_bytes(op, dk, dk, M - 1, in_dtype).total == merge - saved
 
 
 def test_benefit_condition():
     """Eq. 10 benefit condition: DeltaLog moves fewer bytes than eager iff
     C_state (1 - 1/M) > C_log(M) + 2 C_decay; true for M in 2..32 at 128x128 GDN."""
+    eager = T.eager_bytes("gdn", 128, 128).total
     for M in range(2, 33):
-        assert T.amortized_bytes_per_token("gdn", 128, 128, M) < T.eager_bytes("gdn", 128, 128).total
-    assert T.amortized_bytes_per_token("gdn", 128, 128, 1) > T.eager_bytes("gdn", 128, 128).total
+        assert T.amortized_bytes_per_token("gdn", 128, 128, M, stored_ell=True) < eager
+        assert T.amortized_bytes_per_token("gdn", 128, 128, M) < eager
+    # M = 1 is the eager step plus the cumulative log-decay traffic of the paper's
+    # representation; this library keeps none for head-wise decay, so it equals eager
+    assert T.amortized_bytes_per_token("gdn", 128, 128, 1, stored_ell=True) > eager
+    assert T.amortized_bytes_per_token("gdn", 128, 128, 1) == eager
 
 
 def test_byte_optimal_merge_interval():
@@ -77,6 +88,18 @@ def test_byte_optimal_merge_interval():
         a = [T.amortized_bytes_per_token(op, d, d, M) for M in range(1, 65)]
         assert a[m - 1] == min(a)
         assert a[m - 1] < T.eager_bytes(op, d, d).total
+
+
+def test_library_write_ratio_meets_the_bound_for_head_wise_decay():
+    """With one log-decay per head the library writes the live length (4 bytes) where the
+    paper's representation writes the cumulative log-decay (4 bytes): the implied write
+    ratio equals the bound of Eq. 9.  With per-key decay the live length comes on top."""
+    for op, d, M in (("gdn", 128, 16), ("retnet", 128, 16), ("gdn", 64, 8)):
+        assert T.library_state_write_ratio(op, d, d, M) == pytest.approx(
+            T.state_write_ratio(op, d, d, M), rel=1e-12)
+    for op, d, M in (("kda", 128, 16), ("rwkv6", 64, 16), ("gla", 128, 16)):
+        lib, bound = T.library_state_write_ratio(op, d, d, M), T.state_write_ratio(op, d, d, M)
+        assert lib < bound and (bound - lib) / bound < 0.005
 
 
 def test_live_length_metadata_lowers_the_write_ratio_slightly():
