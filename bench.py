@@ -166,9 +166,10 @@ def profile_key(workload, state_dtype, tiled=0, fused_replay=False):
     return key
 
 
-def counter_traffic(key):
-    """HBM bytes per launch of the dominant kernel from the committed counter profile,
-    or None when there is none or the kernel sources changed since it was taken."""
+def counter_profile(key):
+    """The TRAFFIC_JSON record of the committed counter profile of ``key`` (HBM bytes per
+    launch of the dominant kernel, measured state-write ratio), or None when there is
+    none or the kernel code changed since it was taken; and where it came from."""
     path = os.path.join(ROOT, "profiles", f"{key}_hbm_counters.txt")
     if not os.path.exists(path):
         return None, "no counter profile"
@@ -178,7 +179,14 @@ def counter_traffic(key):
     d = json.loads(m.group(1))
     if d.get("kernel_source_hash") != kernel_source_hash():
         return None, "kernel sources changed since the counters were taken"
-    return d["step_kernel_bytes_per_launch"], os.path.relpath(path, ROOT)
+    return d, os.path.relpath(path, ROOT)
+
+
+def counter_traffic(key):
+    """HBM bytes per launch of the dominant kernel from the committed counter profile,
+    or None (see ``counter_profile``)."""
+    d, src = counter_profile(key)
+    return (None if d is None else d["step_kernel_bytes_per_launch"]), src
 
 
 def copy_ceiling(torch, stream, gib=2, reps=5):
@@ -617,8 +625,12 @@ def main():
     eg_us = eg_ms * 1e3 / n_launch
     eg_gbs = eg_bytes / (eg_us * 1e-6) / 1e9
 
-    traffic, traffic_src = counter_traffic(profile_key(args.workload, sd, args.tiled,
-                                                       args.fused_replay))
+    if args.batch or args.merge_interval or args.replicas:
+        prof, traffic_src = None, "no counter profile for this configuration (overrides given)"
+    else:
+        prof, traffic_src = counter_profile(profile_key(args.workload, sd, args.tiled,
+                                                        args.fused_replay))
+    traffic = None if prof is None else prof["step_kernel_bytes_per_launch"]
     copy_gbs = copy_ceiling(torch, stream)
     state_mib = heads * w.dk * w.dv * (2 if sd == "bf16" else 4) / 2**20
     kname = {"gdn": "GDN", "kda": "KDA", "rwkv6": "RWKV6", "linattn": "LinearAttention",
@@ -686,7 +698,11 @@ def main():
             "frac": round(eg_gbs / HBM_PEAK_GBS, 4),
         },
         "speedup_vs_eager": round(dl_tok / eg_tok, 3),
-        "state_write_ratio_model": round(T.state_write_ratio(w.op, w.dk, w.dv, w.M, w.in_dtype, sd), 2),
+        "state_write_ratio_measured": (None if prof is None
+                                       else prof.get("state_write_ratio_measured")),
+        "state_write_ratio_bound": round(T.state_write_ratio(w.op, w.dk, w.dv, w.M, w.in_dtype, sd), 3),
+        "state_write_ratio_layout": round(T.library_state_write_ratio(w.op, w.dk, w.dv, w.M,
+                                                                     w.in_dtype, sd), 3),
         "kernel_source_hash": kernel_source_hash(),
     }
     if not args.no_cpu_baseline:
