@@ -290,8 +290,6 @@ def decode_loop(args):
                 for _ in range(min(per_step, eng.sched.free_slots)):
                     slot = eng.sched.admit()           # the base already holds a state
                     for st in eng.states:
-                        if st.ell is not None:
-                            st.ell[slot].zero_()
                         st.len[slot].zero_()
                 eng.schedule()
                 eng.step()

@@ -24,7 +24,7 @@
  *  - Arrays are dense, row-major, with the shapes given below.  B = desc->num_slots,
  *    H = desc->heads, C = desc->merge_interval - 1 (live-log capacity),
  *    dl = 1 for GDN and RetNet (one log-decay per head), dl = dk for KDA, RWKV6 and
- *    GLA (per key); linear attention has no decay (no ell, lam_log or lam).
+ *    GLA (per key); linear attention has no decay (no lam_log or lam).
  *  - The state matrix of a head is dk x dv, rows indexed by the key dimension; the
  *    decay D(.) scales rows (Eq. 2); outputs are o = x^T S (length dv).
  *  - `slots` is a device int32 array of n distinct slot ids in [0, B): token row i
@@ -90,10 +90,11 @@ typedef enum { DL_F32 = 0, DL_BF16 = 1 } dl_dtype;
  *   RETNET  head-wise scalar decay gamma_t = exp(lambda_t), pair (k, v), o = q^T S_t;
  *   GLA     per-key decay, pair (k, v), o = q^T S_t.
  * dl (the log-decay width) is dk for KDA, RWKV6 and GLA and 1 for GDN and RetNet;
- * linear attention has no log-decay and touches none of ell, lam_log or lam.
- * The cumulative log-decay ell is stored for per-key decay only: with one log-decay per
- * head it always equals the newest snapshot Lam_log[L-1] (Eq. 5 writes both with the
- * same value; 0 when L = 0), and the library reads it from there. */
+ * linear attention has no log-decay and touches neither lam_log nor lam.
+ * The cumulative log-decay ell of Sec. 3.1 is not a buffer here: Eq. 5 writes ell and
+ * the new snapshot Lam_log[L] with the same value and Eq. 6 resets ell together with L,
+ * so ell is always the newest snapshot Lam_log[L-1], or 0 when L = 0, and the library
+ * reads it from there. */
 typedef struct {
   int32_t abi_version;    /* must be DL_ABI_VERSION                                      */
   int32_t op;             /* dl_op                                                       */
@@ -109,12 +110,10 @@ typedef struct {
                           /* every store; every other buffer keeps its dtype)            */
 } dl_desc;
 
-/* DeltaLog physical state (Sec. 3.1 list of buffers), one entry per (slot, head). */
+/* DeltaLog physical state (Sec. 3.1 list of buffers, less ell: see dl_desc), one entry
+ * per (slot, head). */
 typedef struct {
   void*    S;        /* [B,H,dk,dv] state_dtype dense base                               */
-  float*   ell;      /* [B,H,dk]    fp32 cumulative log-decay since the last merge, for  */
-                     /*             KDA, RWKV6, GLA; ignored (may be NULL) for GDN,      */
-                     /*             RetNet (see dl_desc) and LINATTN                     */
   void*    k_log;    /* [B,H,C,dk]  in_dtype   key-side factors   (may be NULL if C == 0) */
   void*    u_log;    /* [B,H,C,dv]  u_log_dtype value-side factors (may be NULL if C == 0)*/
   float*   lam_log;  /* [B,H,C,dl]  fp32 snapshot of ell per entry (may be NULL if C == 0)*/
@@ -145,8 +144,9 @@ int dl_eager_step(const dl_desc* desc, void* S, const dl_token* tok, float* o,
 
 /* One DeltaLog decode step (Alg. 1) for the listed slots: per (slot, head) read the
  * base once, replay the live log, write the output, then append the factors
- * (Eq. 5) if L < C, else merge log and token into the base (Eq. 6) and reset L and
- * ell.  With M == 1 every step merges and the result equals dl_eager_step. */
+ * (Eq. 5) if L < C, else merge log and token into the base (Eq. 6) and reset L (the
+ * cumulative log-decay restarts at 0).  With M == 1 every step merges and the result
+ * equals dl_eager_step. */
 int dl_append_step(const dl_desc* desc, const dl_state* state, const dl_token* tok,
                    float* o, const int32_t* slots, int32_t n, hipStream_t stream);
 
@@ -174,7 +174,7 @@ int dl_readout(const dl_desc* desc, const dl_state* state, const void* q, float*
  *                 the prepared coefficients, or recomputing them per tile when
  *                 split_replay == 0), write the output slice, append the tile's U_log
  *                 shard (tile 0 also writes K_log[L] and Lam_log[L]) or merge the tile;
- *   Finalize      per (row, head): commit L (and ell, where stored) exactly once.
+ *   Finalize      per (row, head): commit L exactly once.
  * value_tiles: 2 or 4.  Only state_dtype == DL_F32 (else DL_E_DTYPE).
  * workspace: device memory of at least dl_tiled_workspace_bytes(desc, n) bytes, 16-byte
  * aligned, owned by the caller; required when split_replay != 0 and C > 0, ignored

@@ -113,8 +113,6 @@ def calibrate(op, B, H, dk, dv, in_dtype="bf16", state_dtype="f32", max_M=64, re
     def at_length(L):
         def prep(st):
             st.len.fill_(L)
-            if st.ell is not None:
-                st.ell.zero_()
         return prep
 
     for st in states:                                    # warm-up of both kernels

@@ -18,9 +18,6 @@ bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p
 
 bool is_delta(int op) { return op == DL_OP_GDN || op == DL_OP_KDA; }
 bool has_decay(int op) { return op != DL_OP_LINATTN; }
-// The cumulative log-decay is stored for per-key decay only (head-wise decay reads it
-// back from the newest Lam_log snapshot).
-bool keeps_ell(int op) { return op == DL_OP_KDA || op == DL_OP_RWKV6 || op == DL_OP_GLA; }
 
 int check_desc(const dl_desc* d) {
   if (!d) return DL_E_NULL;
@@ -69,11 +66,10 @@ int check_token(const dl_desc* d, const dl_token* t) {
 
 int check_state(const dl_desc* d, const dl_state* s) {
   const bool decay = has_decay(d->op);
-  if (!s || !s->S || !s->len || (keeps_ell(d->op) && !s->ell)) return DL_E_NULL;
+  if (!s || !s->S || !s->len) return DL_E_NULL;
   if (d->merge_interval > 1 && (!s->k_log || !s->u_log)) return DL_E_NULL;
   if (d->merge_interval > 1 && decay && !s->lam_log) return DL_E_NULL;
   if (!aligned(s->S, 16) || !aligned(s->len, 4)) return DL_E_ALIGN;
-  if (keeps_ell(d->op) && !aligned(s->ell, 4)) return DL_E_ALIGN;
   if (s->k_log && !aligned(s->k_log, 16)) return DL_E_ALIGN;
   if (s->u_log && !aligned(s->u_log, 16)) return DL_E_ALIGN;
   if (s->lam_log && !aligned(s->lam_log, 4)) return DL_E_ALIGN;
@@ -93,7 +89,6 @@ KParams base_params(const dl_desc* d, const int32_t* slots, int32_t n) {
 
 void set_state(KParams& p, const dl_state* s) {
   p.S = s->S;
-  p.ell = s->ell;
   p.k_log = s->k_log;
   p.u_log = s->u_log;
   p.lam_log = s->lam_log;

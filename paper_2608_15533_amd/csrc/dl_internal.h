@@ -22,7 +22,6 @@ enum ModeId { M_EAGER = 0, M_STEP = 1, M_MERGE = 2, M_FLUSH = 3, M_READOUT = 4 }
 // Everything a kernel needs, passed by value (all pointers are device pointers).
 struct KParams {
   void* S;               // [B,H,dk,dv] dense base (or the eager dense state), fp32 or bf16
-  float* ell;            // [B,H,dl] (unused by linear attention)
   void* k_log;           // [B,H,C,dk]
   void* u_log;           // [B,H,C,dv]
   float* lam_log;        // [B,H,C,dl]

@@ -321,9 +321,6 @@ struct OpTraits {
   static constexpr bool PER_KEY = OP == OP_KDA || OP == OP_RWKV6 || OP == OP_GLA;
   static constexpr bool DECAY = OP != OP_LINATTN;               // linear attention: none
   static constexpr bool BONUS = OP == OP_RWKV6;   // pre-update readout plus r^T diag(u) k v^T
-  // A stored cumulative log-decay (ell): per-key decay only.  For one log-decay per head
-  // it is the newest Lam_log snapshot (0 with an empty log) and is read from there.
-  static constexpr bool KEEPS_ELL = PER_KEY;
 };
 
 template <int OP, int DK, int DV, int MODE>
@@ -342,7 +339,6 @@ struct Cfg {
   static constexpr bool DELTA = OpTraits<OP>::DELTA;
   static constexpr bool DECAY = OpTraits<OP>::DECAY;
   static constexpr bool BONUS = OpTraits<OP>::BONUS;
-  static constexpr bool KEEPS_ELL = OpTraits<OP>::KEEPS_ELL;
   static constexpr bool HAS_LOG = MODE != M_EAGER;
   static constexpr bool HAS_TOKEN = MODE == M_EAGER || MODE == M_STEP || MODE == M_MERGE;
   static constexpr bool READS_OUT = MODE != M_FLUSH;
@@ -462,7 +458,6 @@ void deltalog_kernel(KParams p) {
     if constexpr (CF::BONUS) uf = p.u[size_t(h) * DK + rl];
   }
   if constexpr (CF::READS_OUT) q_raw = qin[rl];
-  if constexpr (CF::HAS_LOG && CF::KEEPS_ELL) ell = p.ell[sh * DL + rd];
   Raw4<TIN> v_raw{};
   float beta = 0.f;
   if constexpr (CF::HAS_TOKEN) {
@@ -502,12 +497,15 @@ void deltalog_kernel(KParams p) {
   const float* Lb = Lw;
   const size_t LS = lam_log_stride<DL>(p);
   const TU* Ub = static_cast<const TU*>(p.u_log) + sh * size_t(C) * DV;
-  // Head-wise decay keeps no separate cumulative log-decay: after an append it equals
-  // the newest snapshot (Eq. 5 writes both with the same value), after a merge it is 0.
-  // Entry L-1 is not written by this launch (the append writes entry L), so it is read
-  // through the scalar path, without waiting for the tile in flight.
-  if constexpr (CF::HAS_LOG && CF::DECAY && !CF::KEEPS_ELL)
-    ell = L > 0 ? scalar_ld(Lb + size_t(L - 1) * LS) : 0.f;
+  // The cumulative log-decay is not stored: after an append it equals the newest
+  // snapshot (Eq. 5 writes both with the same value), after a merge it is 0 (Eq. 6
+  // resets it with L).  Entry L-1 is not written by this launch (an append writes entry
+  // L), so one value per head is read through the scalar path, without waiting for the
+  // tile in flight; per-key values are one vector load per row.
+  if constexpr (CF::HAS_LOG && CF::DECAY) {
+    if constexpr (DL == 1) ell = L > 0 ? scalar_ld(Lb + size_t(L - 1) * LS) : 0.f;
+    else ell = L > 0 ? Lb[size_t(L - 1) * LS + rd] : 0.f;
+  }
   const int e_ = tid / CF::LPE;                   // coefficient pass: entry within the pass
   const int c_ = tid % CF::LPE;                   //                   key-row run
   // Per-key snapshots are prefetched only where the registers allow it (small heads).
@@ -751,7 +749,6 @@ void deltalog_kernel(KParams p) {
       if constexpr (CF::DECAY) {
         for (int x = tid; x < DL; x += NT) {
           Lw[size_t(L) * LS + x] = s_lm[x];
-          if constexpr (CF::KEEPS_ELL) p.ell[sh * DL + x] = s_lm[x];
         }
       }
       if (tid == 0) p.len[sh] = L + 1;
@@ -813,9 +810,7 @@ void deltalog_kernel(KParams p) {
 #pragma unroll
     for (int j = 0; j < RPT; ++j) StateQuad<TS>::store(srs, toff, j * kRowBlock, m[j]);
     if constexpr (CF::HAS_LOG) {
-      if constexpr (CF::KEEPS_ELL)
-        for (int x = tid; x < DL; x += NT) p.ell[sh * DL + x] = 0.f;
-      if (tid == 0) p.len[sh] = 0;
+      if (tid == 0) p.len[sh] = 0;                 // the cumulative log-decay restarts at 0
     }
   }
 }

@@ -11,8 +11,8 @@
 //                       output slice, then either append the tile's U_log[L] shard --
 //                       tile 0 being the designated writer of the shared K_log[L] and
 //                       Lam_log[L] -- or merge the tile's columns of the base;
-//   finalize_kernel     once per (row, head): commit ell and L (append: ell + lambda,
-//                       L + 1; merge: 0, 0) after every tile has read them.
+//   finalize_kernel     once per (row, head): commit L (append: L + 1; merge: 0) after
+//                       every tile has read it.
 //
 // The arithmetic per element is that of dl_kernel.hpp; the coefficient routine is shared
 // by the prepare kernel and the fused tile kernel, so the split and fused variants give
@@ -82,19 +82,20 @@ __device__ __forceinline__ void replay_coefficients(const TIN* Kb, const float* 
   }
 }
 
-// Cumulative log-decay of a (slot, head) at live length L, element x: stored for
-// per-key decay; for one log-decay per head, the newest snapshot (0 with an empty log).
+// Cumulative log-decay of a (slot, head) at live length L, element x: the newest
+// snapshot, 0 with an empty log (it is not stored; see the step kernel).
 template <int OP, int DK>
 __device__ __forceinline__ float cumulative_decay(const KParams& p, size_t sh, int L, int x) {
   using TR = OpTraits<OP>;
   if constexpr (!TR::DECAY) {
     return 0.f;
-  } else if constexpr (TR::KEEPS_ELL) {
-    return p.ell[sh * DK + x];
-  } else {
+  } else if constexpr (!TR::PER_KEY) {
     const int slot = int(sh / size_t(p.H)), h = int(sh % size_t(p.H));
     return L > 0 ? scalar_ld(lam_log_base<1>(p, slot, h) + size_t(L - 1) * lam_log_stride<1>(p))
                  : 0.f;
+  } else {
+    const int slot = int(sh / size_t(p.H)), h = int(sh % size_t(p.H));
+    return L > 0 ? lam_log_base<DK>(p, slot, h)[size_t(L - 1) * DK + x] : 0.f;
   }
 }
 
@@ -326,7 +327,7 @@ void tile_step_kernel(KParams p, const float* __restrict__ coef) {
       if constexpr (TR::DECAY)
         for (int x = tid; x < DL; x += NT) Lw[size_t(L) * LS + x] = s_lm[x];
     }
-    return;                                        // ell and L: finalize_kernel
+    return;                                        // L: finalize_kernel
   }
 
   // ---- merge (Eq. 6) of the tile's columns -------------------------------------------
@@ -376,26 +377,18 @@ void tile_step_kernel(KParams p, const float* __restrict__ coef) {
 }
 
 // ------------------------------------------------------------------ Finalize
-// One wave per (row, head): append -> ell += lambda, L + 1; merge -> ell = 0, L = 0.
-// ell + lambda is the same fp32 sum the tiles used for Lam_log[L].  Head-wise decay
-// stores no ell (it is read back from Lam_log), so only L is committed there.
+// One wave per (row, head): append -> L + 1; merge -> L = 0.  The cumulative log-decay
+// follows from Lam_log[L] (written by tile 0) and L, so L is all there is to commit.
 template <int OP, int DK>
 __global__ __launch_bounds__(64) void finalize_kernel(KParams p) {
-  using TR = OpTraits<OP>;
-  constexpr int DL = TR::PER_KEY ? DK : 1;
   const int tid = threadIdx.x;
   const int row = int(blockIdx.x) / p.H, h = int(blockIdx.x) - row * p.H;
   size_t sh = 0;
   const int L = tiled_row(p, row, h, sh);           // every lane reads L before lane 0 writes it
   if (L < 0) return;                                // invalid: reported by the tiles
-  const size_t th = size_t(row) * p.H + h;
   if (L < p.C) {
-    if constexpr (TR::KEEPS_ELL)
-      for (int x = tid; x < DL; x += 64) p.ell[sh * DL + x] = p.ell[sh * DL + x] + p.lam[th * DL + x];
     if (tid == 0) p.len[sh] = L + 1;
   } else {
-    if constexpr (TR::KEEPS_ELL)
-      for (int x = tid; x < DL; x += 64) p.ell[sh * DL + x] = 0.f;
     if (tid == 0) p.len[sh] = 0;
   }
 }

@@ -43,8 +43,8 @@ list a graph reads is a fixed device buffer that the engine refreshes with one s
 host-to-device copy, outside the graph, when the plan's row order changes.
 
 Slot lifecycle (Sec. 4): ``admit`` writes the prefill state into the slot's dense base
-and resets only the slot's auxiliary buffers (cumulative log-decay, where the operator
-has one, and live length; log rows past the live length are never read).  ``release`` frees the slot, optionally
+and resets only the slot's live length (which also restarts the cumulative log-decay;
+log rows past the live length are never read).  ``release`` frees the slot, optionally
 flushing its log into the base first so the materialised state can be saved.
 """
 
@@ -137,8 +137,6 @@ class DecodeEngine:
                 st.S[slot].zero_()
             else:
                 st.S[slot].copy_(prefill[layer])
-            if st.ell is not None:
-                st.ell[slot].zero_()
             st.len[slot].zero_()
         self.plan = None
         return slot

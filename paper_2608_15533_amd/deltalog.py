@@ -54,7 +54,7 @@ class dl_desc(ctypes.Structure):
 
 
 class dl_state(ctypes.Structure):
-    _fields_ = [("S", ctypes.c_void_p), ("ell", ctypes.c_void_p), ("k_log", ctypes.c_void_p),
+    _fields_ = [("S", ctypes.c_void_p), ("k_log", ctypes.c_void_p),
                 ("u_log", ctypes.c_void_p), ("lam_log", ctypes.c_void_p),
                 ("len", ctypes.c_void_p), ("err", ctypes.c_void_p)]
 
@@ -145,13 +145,12 @@ def _need(t, name, dtype, shape, device=None):
 class DeltaLogState:
     """Device buffers of the physical state (Sec. 3.1), allocated with torch.
 
-    S [B,H,dk,dv] state dtype, ell [B,H,dk] f32 (per-key decay only), k_log [B,H,C,dk]
-    in_dtype, u_log [B,H,C,dv], lam_log [B,H,C,dl] f32 ([B,C,H] for one log-decay per
-    head), len [B,H] int32, err [1] int32.  ``S`` starts as a copy of ``S0`` (the
-    prefill state, converted to the state dtype); the log starts empty (Sec. 4 slot
-    lifecycle).  With one log-decay per head (GDN, RetNet) the cumulative log-decay is
-    the newest snapshot and ``ell`` is None; linear attention has no decay, so ``ell``
-    and ``lam_log`` are None.  None buffers are passed to the library as NULL.
+    S [B,H,dk,dv] state dtype, k_log [B,H,C,dk] in_dtype, u_log [B,H,C,dv], lam_log
+    [B,H,C,dl] f32 ([B,C,H] for one log-decay per head), len [B,H] int32, err [1] int32.
+    ``S`` starts as a copy of ``S0`` (the prefill state, converted to the state dtype);
+    the log starts empty (Sec. 4 slot lifecycle).  The cumulative log-decay of Sec. 3.1
+    is not a buffer: it is the newest snapshot (0 with an empty log), which the kernels
+    read.  Linear attention has no decay, so ``lam_log`` is None (NULL to the library).
     """
 
     def __init__(self, desc, S0=None, device="cuda"):
@@ -165,9 +164,6 @@ class DeltaLogState:
         st = state_torch_dtype(desc)
         self.S = (torch.zeros((B, H, dk, dv), dtype=st, device=device) if S0 is None else
                   S0.to(device=device, dtype=st).contiguous().clone())
-        # the cumulative log-decay is stored for per-key decay only; with one log-decay
-        # per head the library reads it from the newest Lam_log snapshot
-        self.ell = torch.zeros((B, H, dl), **f32) if dl > 1 else None
         self.k_log = torch.zeros((B, H, max(C, 0), dk), dtype=in_t, device=device)
         self.u_log = torch.zeros((B, H, max(C, 0), dv), dtype=u_t, device=device)
         # scalar snapshots are entry-major [B, C, H] (the heads of a slot side by side)
@@ -177,14 +173,14 @@ class DeltaLogState:
             self.lam_log = torch.zeros((B, H, max(C, 0), dl), **f32) if dl else None
         self.len = torch.zeros((B, H), dtype=torch.int32, device=device)
         self.err = torch.zeros((1,), dtype=torch.int32, device=device)
-        self.struct = dl_state(_ptr(self.S), _ptr(self.ell),
+        self.struct = dl_state(_ptr(self.S),
                                _ptr(self.k_log) if C > 0 else None,
                                _ptr(self.u_log) if C > 0 else None,
                                _ptr(self.lam_log) if C > 0 and dl else None,
                                _ptr(self.len), _ptr(self.err))
 
     def buffers(self):
-        return dict(S=self.S, ell=self.ell, k_log=self.k_log, u_log=self.u_log,
+        return dict(S=self.S, k_log=self.k_log, u_log=self.u_log,
                     lam_log=self.lam_log, len=self.len, err=self.err)
 
 

@@ -16,9 +16,9 @@ phase, with the precisions the library uses:
   activation dtype for the others (exact copies of v).
 * cumulative log-decay ``C_decay``: 4 d_lambda bytes, read and written every DeltaLog step
   in the paper's representation (d_lambda = 0 for linear attention: no decay, no
-  snapshots).  This library stores it for per-key decay only: with one log-decay per
-  head it equals the newest snapshot, which the replay reads anyway, so the step moves
-  no separate ``C_decay`` bytes (``stored_ell=None`` selects the library's layout,
+  snapshots).  This library stores no such buffer: the cumulative log-decay equals the
+  newest snapshot, which the replay reads anyway, so its steps move no separate
+  ``C_decay`` bytes (``stored_ell=False``, the default, is the library's layout;
   ``True`` the paper's).
 * the output o: fp32, dv values.
 * live-length and index metadata are omitted as lower-order, as the paper does.
@@ -31,7 +31,7 @@ Per phase (one head, one token):
     merge at L   read  T_common + C_state + C_decay + L C_entry
                  write C_state + C_decay + o
 
-(C_decay counted only where the cumulative log-decay is stored.)
+(C_decay counted only in the paper's representation, ``stored_ell=True``.)
 """
 
 from dataclasses import dataclass
@@ -70,38 +70,32 @@ def eager_bytes(op, dk, dv, in_dtype="bf16", state_dtype="f32"):
     return HeadTraffic(read=common + state, write=state + out)
 
 
-def stores_ell(op):
-    """Whether this library keeps a cumulative log-decay buffer for ``op`` (per-key decay
-    only; with one log-decay per head it is the newest snapshot)."""
-    return op in PER_KEY_OPS
+def _ell(decay, stored_ell):
+    return decay if stored_ell else 0
 
 
-def _ell(op, decay, stored_ell):
-    return decay if (stores_ell(op) if stored_ell is None else stored_ell) else 0
-
-
-def append_bytes(op, dk, dv, L, in_dtype="bf16", state_dtype="f32", stored_ell=None):
+def append_bytes(op, dk, dv, L, in_dtype="bf16", state_dtype="f32", stored_ell=False):
     """Bytes of a DeltaLog append step taken at live length L."""
     common, state, entry, decay, out = _sizes(op, dk, dv, in_dtype, state_dtype)
-    ell = _ell(op, decay, stored_ell)
+    ell = _ell(decay, stored_ell)
     return HeadTraffic(read=common + state + ell + L * entry, write=entry + ell + out)
 
 
-def merge_bytes(op, dk, dv, L, in_dtype="bf16", state_dtype="f32", stored_ell=None):
+def merge_bytes(op, dk, dv, L, in_dtype="bf16", state_dtype="f32", stored_ell=False):
     """Bytes of a DeltaLog merge step that folds L live entries (plus the token)."""
     common, state, entry, decay, out = _sizes(op, dk, dv, in_dtype, state_dtype)
-    ell = _ell(op, decay, stored_ell)
+    ell = _ell(decay, stored_ell)
     return HeadTraffic(read=common + state + ell + L * entry, write=state + ell + out)
 
 
-def step_bytes(op, dk, dv, M, L, in_dtype="bf16", state_dtype="f32", stored_ell=None):
+def step_bytes(op, dk, dv, M, L, in_dtype="bf16", state_dtype="f32", stored_ell=False):
     """Bytes of the Alg. 1 step at live length L: append if L < M-1, else merge."""
     if L < M - 1:
         return append_bytes(op, dk, dv, L, in_dtype, state_dtype, stored_ell)
     return merge_bytes(op, dk, dv, L, in_dtype, state_dtype, stored_ell)
 
 
-def cycle_bytes(op, dk, dv, M, in_dtype="bf16", state_dtype="f32", stored_ell=None):
+def cycle_bytes(op, dk, dv, M, in_dtype="bf16", state_dtype="f32", stored_ell=False):
     """Total bytes of one full cycle (M-1 appends at L = 0..M-2, one merge at L = M-1)."""
     r = w = 0
     for L in range(M):
@@ -112,7 +106,7 @@ def cycle_bytes(op, dk, dv, M, in_dtype="bf16", state_dtype="f32", stored_ell=No
 
 
 def amortized_bytes_per_token(op, dk, dv, M, in_dtype="bf16", state_dtype="f32",
-                              stored_ell=None):
+                              stored_ell=False):
     """Average bytes per head-token over a cycle (the Eq. 10 quantity, plus outputs)."""
     c = cycle_bytes(op, dk, dv, M, in_dtype, state_dtype, stored_ell)
     return c.total / M
@@ -124,19 +118,19 @@ def state_write_ratio(op, dk, dv, M, in_dtype="bf16", state_dtype="f32", live_le
     this is the bound of Eq. 9, M / (1 + eps), in the paper's representation (the
     cumulative log-decay written every step).  ``live_length_bytes`` adds the per-step
     write of the live length (metadata the paper's model omits; 4 for the int32 length
-    this library keeps per slot and head); ``stored_ell=None`` counts the cumulative
-    log-decay only where this library stores it."""
+    this library keeps per slot and head); ``stored_ell=False`` leaves out the
+    cumulative log-decay, which this library does not store."""
     _, state, entry, decay, _ = _sizes(op, dk, dv, in_dtype, state_dtype)
-    ell = _ell(op, decay, stored_ell)
+    ell = _ell(decay, stored_ell)
     dl_writes = (state + (M - 1) * entry + M * (ell + live_length_bytes)) / M
     return state / dl_writes
 
 
 def library_state_write_ratio(op, dk, dv, M, in_dtype="bf16", state_dtype="f32"):
-    """The write ratio this library's layout implies: the log entries, the cumulative
-    log-decay where it is stored, and the 4-byte live length of every head-step."""
+    """The write ratio this library's layout implies: the log entries and the 4-byte live
+    length of every head-step (no cumulative log-decay buffer)."""
     return state_write_ratio(op, dk, dv, M, in_dtype, state_dtype, live_length_bytes=4,
-                             stored_ell=None)
+                             stored_ell=False)
 
 
 def byte_optimal_merge_interval(op, dk, dv, in_dtype="bf16", state_dtype="f32", max_M=64):

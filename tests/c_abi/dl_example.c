@@ -73,7 +73,7 @@ int dl_example_run(double* max_rel_err) {
   double worst = 0.0;
   float *hS = NULL, *hq = NULL, *hk = NULL, *hv = NULL, *hlam = NULL, *hbeta = NULL;
   float *ho = NULL, *hoe = NULL, *hS2 = NULL;
-  float *S = NULL, *Se = NULL, *ell = NULL, *u_log = NULL, *lam_log = NULL;
+  float *S = NULL, *Se = NULL, *u_log = NULL, *lam_log = NULL;
   float *q = NULL, *k = NULL, *v = NULL, *lam = NULL, *beta = NULL, *o = NULL, *oe = NULL;
   float *k_log = NULL;
   int32_t *len = NULL, *err = NULL, herr = 0;
@@ -86,7 +86,6 @@ int dl_example_run(double* max_rel_err) {
 
   HIP_TRY(hipMalloc((void**)&S, nS * 4));
   HIP_TRY(hipMalloc((void**)&Se, nS * 4));
-  HIP_TRY(hipMalloc((void**)&ell, nbh * 4));
   HIP_TRY(hipMalloc((void**)&k_log, nbh * C * DK * 4));
   HIP_TRY(hipMalloc((void**)&u_log, nbh * C * DV * 4));
   HIP_TRY(hipMalloc((void**)&lam_log, nbh * C * 4));          /* dl = 1: [B, C, H] */
@@ -101,8 +100,7 @@ int dl_example_run(double* max_rel_err) {
   HIP_TRY(hipMalloc((void**)&oe, nv * 4));
   HIP_TRY(hipMemcpy(S, hS, nS * 4, hipMemcpyHostToDevice));
   HIP_TRY(hipMemcpy(Se, hS, nS * 4, hipMemcpyHostToDevice));
-  HIP_TRY(hipMemset(ell, 0, nbh * 4));                        /* empty log: ell = 0, L = 0 */
-  HIP_TRY(hipMemset(len, 0, nbh * 4));
+  HIP_TRY(hipMemset(len, 0, nbh * 4));                        /* empty log: L = 0 */
   HIP_TRY(hipMemset(err, 0, 4));
 
   {
@@ -118,7 +116,7 @@ int dl_example_run(double* max_rel_err) {
     d.in_dtype = DL_F32;
     d.u_log_dtype = DL_F32;
     d.state_dtype = DL_F32;
-    dl_state st = {S, ell, k_log, u_log, lam_log, len, err};
+    dl_state st = {S, k_log, u_log, lam_log, len, err};
     dl_token tok = {q, k, v, beta, lam, NULL};
 
     for (int t = 0; t < STEPS; ++t) {
@@ -158,7 +156,7 @@ int dl_example_run(double* max_rel_err) {
 
 done:
   if (max_rel_err) *max_rel_err = worst;
-  hipFree(S); hipFree(Se); hipFree(ell); hipFree(k_log); hipFree(u_log); hipFree(lam_log);
+  hipFree(S); hipFree(Se); hipFree(k_log); hipFree(u_log); hipFree(lam_log);
   hipFree(len); hipFree(err); hipFree(q); hipFree(k); hipFree(v); hipFree(lam);
   hipFree(beta); hipFree(o); hipFree(oe);
   free(hS); free(hS2); free(hq); free(hk); free(hv); free(hlam); free(hbeta); free(ho);

@@ -51,7 +51,7 @@ def desc(**kw):
 
 
 def state(**kw):
-    s = D.dl_state(A, A + 0x100000, A + 0x200000, A + 0x300000, A + 0x400000, A + 0x500000, None)
+    s = D.dl_state(A, A + 0x200000, A + 0x300000, A + 0x400000, A + 0x500000, None)
     for k, v in kw.items():
         setattr(s, k, v)
     return s
@@ -126,24 +126,11 @@ def test_state_nulls(field):
     assert append(desc(), s=state(**{field: None})) == D.DL_E_NULL
 
 
-@pytest.mark.parametrize("op", ["kda", "rwkv6", "gla"])
-def test_per_key_decay_needs_the_cumulative_log_decay(op):
-    d = D.make_desc(op, 4, 2, 128, 128, 16, "bf16")
-    t = token(beta=None) if op != "kda" else token()
-    if op == "rwkv6":
-        t = token(beta=None, u=A + 0xC00000)
-    assert append(d, s=state(ell=None), t=t) == D.DL_E_NULL
-    assert append(d, s=state(ell=A + 0x100002), t=t) == D.DL_E_ALIGN
-
-
-@pytest.mark.parametrize("op", ["gdn", "retnet"])
-def test_head_wise_decay_ignores_the_cumulative_log_decay(op):
-    """One log-decay per head: ell is read back from the newest snapshot, so a NULL or
-    misaligned ell passes the checks (the call then stops at the misaligned output)."""
-    d = D.make_desc(op, 4, 2, 128, 128, 16, "bf16")
-    t = token() if op == "gdn" else token(beta=None)
-    assert append(d, s=state(ell=None), t=t, o=A + 4) == D.DL_E_ALIGN
-    assert append(d, s=state(ell=A + 0x100002), t=t, o=A + 4) == D.DL_E_ALIGN
+def test_state_has_no_cumulative_log_decay_buffer():
+    """The cumulative log-decay is the newest Lam_log snapshot, not a buffer: dl_state
+    holds S, the three log buffers, the live length and the error word."""
+    assert [f for f, _ in D.dl_state._fields_] == ["S", "k_log", "u_log", "lam_log", "len",
+                                                    "err"]
 
 
 def test_log_buffers_optional_when_M_is_1():
@@ -165,10 +152,10 @@ def test_rwkv6_needs_bonus():
 
 
 def test_linear_attention_takes_no_decay_buffers():
-    """Linear attention has no decay: NULL lam, ell and lam_log (and beta) pass the checks
+    """Linear attention has no decay: NULL lam and lam_log (and beta) pass the checks
     (the call then stops at the misaligned output)."""
     d = D.make_desc("linattn", 4, 2, 128, 128, 16, "bf16")
-    s = state(ell=None, lam_log=None)
+    s = state(lam_log=None)
     assert append(d, s=s, t=token(lam=None, beta=None), o=A + 4) == D.DL_E_ALIGN
     assert append(d, s=state(k_log=None), t=token(lam=None, beta=None)) == D.DL_E_NULL
 
@@ -178,8 +165,6 @@ def test_decaying_additive_operators_need_lam_not_beta(op):
     d = D.make_desc(op, 4, 2, 128, 128, 16, "bf16")
     assert append(d, t=token(beta=None), o=A + 4) == D.DL_E_ALIGN
     assert append(d, t=token(lam=None, beta=None)) == D.DL_E_NULL
-    if op == "gla":
-        assert append(d, s=state(ell=None), t=token(beta=None)) == D.DL_E_NULL
     assert append(d, s=state(lam_log=None), t=token(beta=None)) == D.DL_E_NULL
 
 

@@ -18,8 +18,7 @@ O_BAD = A + 0xB00004                                  # misaligned output: never
 
 
 def _state():
-    return D.dl_state(A, A + 0x100000, A + 0x200000, A + 0x300000, A + 0x400000,
-                      A + 0x500000, None)
+    return D.dl_state(A, A + 0x200000, A + 0x300000, A + 0x400000, A + 0x500000, None)
 
 
 def _token():

@@ -191,9 +191,9 @@ def test_batch_composition_invariance(op):
 
 @pytest.mark.parametrize("op", OPS)
 def test_log_contents_match_the_model(op):
-    """After L appends the log holds: K_log = k bitwise (exact copies), Lam_log and ell =
-    the cumulative log-decay (ell stored for per-key decay, the newest Lam_log entry for
-    head-wise decay, none for linear attention), U_log = the delta-rule values b
+    """After L appends the log holds: K_log = k bitwise (exact copies), Lam_log = the
+    cumulative log-decay at each entry, its newest entry = the model's ell (none for
+    linear attention), U_log = the delta-rule values b
     (GDN/KDA) or v bitwise (the others), len = L -- compared with the fp64 Alg. 1 model."""
     w = WL[op].with_(B=3)
     M, steps = 8, 5
@@ -214,18 +214,14 @@ def test_log_contents_match_the_model(op):
     K = a["k_log"].astype(np.float64).reshape(N, M - 1, w.dk)[:, :L]
     np.testing.assert_array_equal(K, model.K[:, :L])
     if op == "linattn":
-        assert "lam_log" not in a and "ell" not in a
+        assert "lam_log" not in a
     else:
         lam_log = a["lam_log"]
         if lam_log.ndim == 3:               # scalar snapshots: entry-major [B, C, H]
             lam_log = lam_log.transpose(0, 2, 1)[..., None]
         lam_log = lam_log.reshape(N, M - 1, -1)
         assert rel(lam_log[:, :L], model.Lam[:, :L]) <= 1e-6
-        if "ell" in a:                      # stored for per-key decay
-            assert rel(a["ell"].reshape(N, -1), model.ell) <= 1e-6
-        else:                               # one log-decay per head: the newest snapshot
-            assert op in ("gdn", "retnet")
-            assert rel(lam_log[:, L - 1], model.ell) <= 1e-6
+        assert rel(lam_log[:, L - 1], model.ell) <= 1e-6    # ell: the newest snapshot
     U = a["u_log"].astype(np.float64).reshape(N, M - 1, w.dv)[:, :L]
     if op not in OE.DELTA_OPS:
         np.testing.assert_array_equal(U, model.U[:, :L])
@@ -265,7 +261,6 @@ def test_readout_forced_merge_flush(op):
     assert rel(o.cpu().numpy(), ref_o[5]) <= TOL_F32_STATE
     assert rel(st.S.cpu().numpy(), ref_S[5]) <= TOL_F32_STATE
     assert np.all(st.len.cpu().numpy() == 0)
-    assert st.ell is None or np.all(st.ell.cpu().numpy() == 0)
     # three appends then a flush
     for t in (6, 7, 8):
         dl.dl_append_step(desc, st, token(desc, xs[t], u), o)
@@ -273,7 +268,6 @@ def test_readout_forced_merge_flush(op):
     torch.cuda.synchronize()
     assert rel(st.S.cpu().numpy(), ref_S[8]) <= TOL_F32_STATE
     assert np.all(st.len.cpu().numpy() == 0)
-    assert st.ell is None or np.all(st.ell.cpu().numpy() == 0)
     # a flush of an empty log changes nothing
     S_now = st.S.cpu().numpy().copy()
     dl.dl_merge(desc, st)

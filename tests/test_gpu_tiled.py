@@ -95,7 +95,7 @@ def test_split_replay_is_bitwise_fused_replay(op):
 
 @pytest.mark.parametrize("op", list(WL))
 def test_tiled_log_metadata_matches_untiled(op):
-    """After appends, the single-writer entries (K_log, Lam_log), the finalized ell and L
+    """After appends, the single-writer entries (K_log, Lam_log) and the finalized L
     equal the untiled kernel's bit for bit; U_log and outputs agree to the bar (bitwise
     where U_log is a copy of v)."""
     w = WL[op].with_(B=3)
@@ -106,7 +106,7 @@ def test_tiled_log_metadata_matches_untiled(op):
     desc = D().make_desc(op, w.B, w.H, w.dk, w.dv, M, w.in_dtype)
     ot, bt = _run_tiled(desc, S0, xs, u, 2, True)
     ou, bu = _run_tiled(desc, S0, xs, u, 0, False, untiled=True)
-    for k in ("k_log", "lam_log", "ell", "len", "S", "err"):
+    for k in ("k_log", "lam_log", "len", "S", "err"):
         if bu[k] is not None:
             np.testing.assert_array_equal(bt[k], bu[k], err_msg=k)
     L = steps
