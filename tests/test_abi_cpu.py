@@ -250,3 +250,16 @@ def test_tiled_rejections():
     assert tiled(desc(), n=0, nv=4, ws=None) == D.DL_OK   # n == 0: no-op
     assert tiled(desc(), s=state(len=None)) == D.DL_E_NULL
     assert tiled(desc(), t=token(beta=None)) == D.DL_E_NULL
+
+
+def test_binding_refuses_to_load_without_the_library(tmp_path):
+    """No non-HIP fallback: with the library absent, importing the binding (and the
+    decode engine above it) raises ImportError instead of computing anything."""
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    env = dict(os.environ, DELTALOG_LIB=str(tmp_path / "absent" / "libdeltalog.so"))
+    for mod in ("paper_2608_15533_amd.deltalog", "paper_2608_15533_amd.decode"):
+        r = subprocess.run([sys.executable, "-c", f"import {mod}"], cwd=root, env=env,
+                           capture_output=True, text=True, timeout=300)
+        assert r.returncode != 0, mod
+        assert "ImportError" in r.stderr and "no non-HIP fallback" in r.stderr, r.stderr[-400:]
