@@ -18,7 +18,7 @@ values do not change the cost of any kernel.
 
 Besides the contract fields the JSON line carries: the eager dense baseline
 (dl_eager_step on the same states), the per-phase split (append at each live length,
-merge; a separate pass with an event pair around every launch), the roofline entry of
+merge; a separate pass with an event pair around each step's launches), the roofline entry of
 the dominant kernel (algorithmic bytes of the average launch over its average duration,
 the duration taken from HIP events around the timed region on the launch stream), the
 HBM traffic of that kernel from the committed counter profile when the kernel sources
@@ -509,17 +509,15 @@ def main():
                   outs[r].data_ptr(), None, w.B, sp) for t in range(POOL)] for r in range(R)]
 
     def run(fn, argtab, k0, nsteps, events=None):
-        i = 0
-        for k in range(k0, k0 + nsteps):
+        for i, k in enumerate(range(k0, k0 + nsteps)):
+            if events is not None:
+                events[i][0].record(stream)
             for r in range(R):
-                if events is not None:
-                    events[i][0].record(stream)
                 rc = fn(*argtab[r][k % POOL])
                 if rc != 0:
                     raise D.DeltaLogError(rc, fn.__name__)
-                if events is not None:
-                    events[i][1].record(stream)
-                i += 1
+            if events is not None:
+                events[i][1].record(stream)
 
     def with_stream(argtab, handle):
         return [[a[:-1] + (handle,) for a in row] for row in argtab]
@@ -562,13 +560,15 @@ def main():
         return t0.elapsed_time(t1)
 
     def per_launch(fn, argtab, k0, nsteps):
-        """A separate pass with an event pair around every launch (per-phase split);
-        the events are created beforehand so the host keeps ahead of the device."""
+        """A separate pass with an event pair around each step's R launches, which share
+        one live length (per-phase split): returns the mean launch time of every step, so
+        the cost of recording events is spread over R launches instead of inflating each.
+        The events are created beforehand so the host keeps ahead of the device."""
         evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-               for _ in range(nsteps * R)]
+               for _ in range(nsteps)]
         run(fn, argtab, k0, nsteps, evs)
         torch.cuda.synchronize()
-        return np.array([a.elapsed_time(b) for a, b in evs]).reshape(nsteps, R)
+        return np.array([a.elapsed_time(b) for a, b in evs]) / R
 
     def launch_bytes(k):
         """Algorithmic bytes of one layer launch at step k (every slot at its own L)."""
@@ -591,7 +591,8 @@ def main():
     ph_durs = per_launch(app, app_args, k0, PH)
     for s in states:
         assert int(s.err.item()) == 0
-    phases = {"source": "separate pass, HIP event pair around each launch, median per phase"}
+    phases = {"source": "separate pass, HIP event pair around each step's launches (one per "
+                        "layer state, all at one live length), median per phase"}
     if not w.staggered:
         by_L = {}
         for L in range(w.M):
