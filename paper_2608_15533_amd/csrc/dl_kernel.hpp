@@ -111,6 +111,10 @@ __device__ __forceinline__ float dl_exp(float x) { return __expf(x); }
 #ifndef DL_PREFETCH_PER_KEY_SMALL
 #define DL_PREFETCH_PER_KEY_SMALL 1
 #endif
+// ... and for a bf16 state, whose tile holds half the registers of an fp32 one.
+#ifndef DL_PREFETCH_PER_KEY_BF16_STATE
+#define DL_PREFETCH_PER_KEY_BF16_STATE 1
+#endif
 // Issue order of the log entries relative to the state tile (see the kernel).
 #ifndef DL_LOG_FIRST
 #define DL_LOG_FIRST 0
@@ -508,8 +512,10 @@ void deltalog_kernel(KParams p) {
   }
   const int e_ = tid / CF::LPE;                   // coefficient pass: entry within the pass
   const int c_ = tid % CF::LPE;                   //                   key-row run
-  // Per-key snapshots are prefetched only where the registers allow it (small heads).
-  constexpr bool kPrefetchPerKey = DL_PREFETCH_PER_KEY || (DL_PREFETCH_PER_KEY_SMALL && RPT <= 8);
+  // Per-key snapshots are prefetched only where the registers allow it (small heads, or
+  // a bf16 state).
+  constexpr bool kPrefetchPerKey = DL_PREFETCH_PER_KEY || (DL_PREFETCH_PER_KEY_SMALL && RPT <= 8) ||
+                                   (DL_PREFETCH_PER_KEY_BF16_STATE && sizeof(TS) == 2 && RPL <= 8);
   float kr[RPL], lr_[(DL == 1) ? 1 : RPL];
   RawRun<TIN, RPL> kr_raw{};
   RawRun<float, (DL == 1) ? 8 : RPL> lr_raw{};      // per-key snapshots (unused for DL == 1)
