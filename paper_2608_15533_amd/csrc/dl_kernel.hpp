@@ -9,9 +9,10 @@
 // eager / flush), written back exactly once from the same registers -- the read, the
 // key-dimension reductions and the write never leave the workgroup.  Because one
 // workgroup owns all of a head's value columns, the replay coefficients are computed
-// once per (slot, head) and the shared log metadata (K_log[L], Lam_log[L], ell, L) has
-// a single writer without any cross-workgroup finalisation (the ownership problem of
-// Sec. 3.3).
+// once per (slot, head) and the shared log metadata (K_log[L], Lam_log[L], L) has a
+// single writer without any cross-workgroup finalisation (the ownership problem of
+// Sec. 3.3).  The cumulative log-decay ell is not stored: it equals the newest snapshot
+// Lam_log[L-1], or 0 with an empty log.
 //
 // Modes (one template per mode; the per-slot append/merge branch of Alg. 1 is taken
 // on the device from that slot's live length):
