@@ -11,7 +11,7 @@ from oracle import eager as OE
 from oracle.deltalog_model import DeltaLogModel
 from paper_2608_15533_amd import workloads as W
 
-from gpu_harness import TOL_F32_STATE, D, log, oracle_step, rel, to_dev, token
+from gpu_harness import TOL_BF16_STATE, TOL_F32_STATE, D, log, oracle_step, rel, to_dev, token
 
 pytestmark = pytest.mark.gpu
 
@@ -290,6 +290,27 @@ def test_rectangular_heads(op, dk, dv):
     D().dl_merge(desc, st)
     torch.cuda.synchronize()
     assert rel(st.S.cpu().numpy(), ref_S[-1]) <= TOL_F32_STATE
+
+
+@pytest.mark.parametrize("dk,dv", [(64, 128), (128, 64), (128, 128)])
+@pytest.mark.parametrize("op", ["kda", "gla", "gdn"])
+def test_bf16_state_head_shapes(op, dk, dv):
+    """bf16 state on every head layout that prefetches its per-key snapshots (64x128,
+    128x128) or does not (128x64), two merge cycles and a flush, against the fp64 oracle
+    started from the same bf16-rounded state; the bf16-state bar."""
+    log(f"bf16 state {op} {dk}x{dv}")
+    w = W.Workload("bf16shape", 78, op, 3, 4, dk, dv, 4, 11)
+    S0 = W.round_bf16(W.initial_state(w))
+    xs = [W.step_inputs(w, t) for t in range(w.steps)]
+    u = W.bonus(w)
+    desc = D().make_desc(op, w.B, w.H, dk, dv, w.M, w.in_dtype, "bf16")
+    outs, st = run_deltalog(desc, S0, xs, u)
+    ref_o, ref_S = oracle_run(op, S0, xs, u)
+    assert max(rel(a, b) for a, b in zip(outs, ref_o)) <= TOL_BF16_STATE
+    D().dl_merge(desc, st)
+    torch.cuda.synchronize()
+    assert int(st.err.item()) == 0
+    assert rel(st.S.float().cpu().numpy(), ref_S[-1]) <= TOL_BF16_STATE
 
 
 @pytest.mark.parametrize("op", OPS)
