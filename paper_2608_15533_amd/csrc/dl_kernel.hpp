@@ -116,6 +116,15 @@ __device__ __forceinline__ float dl_exp(float x) { return __expf(x); }
 #ifndef DL_PREFETCH_PER_KEY_BF16_STATE
 #define DL_PREFETCH_PER_KEY_BF16_STATE 1
 #endif
+// Row order of the staged K~ chunk in LDS: key row r = c * RPL + x (run c of the
+// coefficient pass, element x of the run) is kept at row x * LPE + c (1), or at r (0).
+// The coefficient pass writes one entry of RPL consecutive rows per lane; in key order
+// the lanes of a wave would meet in a few LDS banks, in this order their rows differ by
+// the run index instead.  The contraction's reads of row rg + NRG j stay at offsets
+// that are constant per j.
+#ifndef DL_KT_ROW_ORDER
+#define DL_KT_ROW_ORDER 1
+#endif
 // Issue order of the log entries relative to the state tile (see the kernel).
 #ifndef DL_LOG_FIRST
 #define DL_LOG_FIRST 0
@@ -356,7 +365,28 @@ struct Cfg {
   static_assert(NT % LPE == 0 && DK % LPE == 0, "coefficient pass layout");
   static_assert(NT >= DK, "one thread per key row in the prologue");
   static_assert(RPL == 4 || RPL == 8 || RPL == 16, "coefficient pass run length");
+  static_assert(NRG % RPL == 0 || RPL % NRG == 0, "row groups and coefficient runs nest");
   static_assert(CH == EPP, "the first merge chunk is staged by the first coefficient pass");
+  // LDS row of key row r in the staged K~ chunk (a permutation of [0, DK)), and the
+  // same for the two ways the kernel names a row: element x of coefficient run c, and
+  // row j of row group rg (rg + NRG j), written so that the part that depends on x or j
+  // is a compile-time constant.
+  static __device__ __forceinline__ int kt_row(int r) {
+    return DL_KT_ROW_ORDER ? (r % RPL) * LPE + r / RPL : r;
+  }
+  static __device__ __forceinline__ int kt_row_run(int c, int x) {
+    return DL_KT_ROW_ORDER ? x * LPE + c : c * RPL + x;
+  }
+  static __device__ __forceinline__ int kt_row_group(int rg, int j) {
+    if constexpr (!DL_KT_ROW_ORDER) {
+      return rg + NRG * j;
+    } else if constexpr (NRG % RPL == 0) {
+      return (rg % RPL) * LPE + rg / RPL + (NRG / RPL) * j;
+    } else {
+      constexpr int q = RPL / NRG;                  // RPL is a multiple of NRG
+      return (rg + NRG * (j % q)) * LPE + j / q;
+    }
+  }
   static_assert(LPE <= 64 && 64 % LPE == 0, "an entry's lanes share one wave");
   static_assert(NT == threads_per_head(DK, DV), "launch bound must match the layout");
   static_assert(!(BONUS && DL == 1), "the bonus readout is only defined with per-key decay");
@@ -632,7 +662,9 @@ void deltalog_kernel(KParams p) {
           aq *= w;
           if (stage) {
 #pragma unroll
-            for (int x = 0; x < RPL; ++x) s_kt[(c_ * RPL + x) * CF::KTS + e_] = w * kr[x];
+            for (int x = 0; x < RPL; ++x) {
+              s_kt[CF::kt_row_run(c_, x) * CF::KTS + e_] = w * kr[x];
+            }
           }
         } else {
 #pragma unroll 2
@@ -641,12 +673,16 @@ void deltalog_kernel(KParams p) {
             const float wk = dl_exp(s_lr[r] - lr_[x]) * kr[x];
             if constexpr (CF::NEEDS_C) ak = fmaf(wk, s_kf[r], ak);
             aq = fmaf(wk, s_qf[r], aq);
-            if (stage) s_kt[r * CF::KTS + e_] = CF::BONUS ? dl_exp(s_lm[r] - lr_[x]) * kr[x] : wk;
+            if (stage)
+              s_kt[CF::kt_row_run(c_, x) * CF::KTS + e_] =
+                  CF::BONUS ? dl_exp(s_lm[r] - lr_[x]) * kr[x] : wk;
           }
         }
       } else if (stage) {
 #pragma unroll
-        for (int x = 0; x < RPL; ++x) s_kt[(c_ * RPL + x) * CF::KTS + e_] = 0.f;
+        for (int x = 0; x < RPL; ++x) {
+          s_kt[CF::kt_row_run(c_, x) * CF::KTS + e_] = 0.f;
+        }
       }
 #pragma unroll
       for (int m = CF::LPE / 2; m >= 1; m >>= 1) {
@@ -789,7 +825,7 @@ void deltalog_kernel(KParams p) {
               val *= dl_exp(s_lm[(DL == 1) ? 0 : r] - lam_i);
             }
           }
-          s_kt[r * CF::KTS + ii] = val;             // K~_i[r] = e^(l'_r - Lam_i,r) K_i[r]
+          s_kt[CF::kt_row(r) * CF::KTS + ii] = val;  // K~_i[r] = e^(l'_r - Lam_i,r) K_i[r]
         }
         for (int x = tid; x < CF::CH * NCG; x += NT) {
           const int ii = x / NCG, c4 = x % NCG;
@@ -804,8 +840,8 @@ void deltalog_kernel(KParams p) {
           const float4 u3 = s_u[(ii + 3) * NCG + cg];
 #pragma unroll
           for (int j = 0; j < RPT; ++j) {
-            const int r = rg + NRG * j;
-            const float4 kt = *reinterpret_cast<const float4*>(&s_kt[r * CF::KTS + ii]);
+            const float4 kt =
+                *reinterpret_cast<const float4*>(&s_kt[CF::kt_row_group(rg, j) * CF::KTS + ii]);
             m[j] = fma4(kt.x, u0, m[j]);
             m[j] = fma4(kt.y, u1, m[j]);
             m[j] = fma4(kt.z, u2, m[j]);
