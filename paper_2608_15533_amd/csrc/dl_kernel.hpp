@@ -85,6 +85,33 @@ __device__ __forceinline__ float4 fma4(float s, float4 b, float4 a) {
 
 __device__ __forceinline__ float shfl_xor(float v, int m) { return __shfl_xor(v, m, 64); }
 
+// Sum over aligned groups of N lanes (N = 4, 8 or 16), every lane of a group ending with
+// the group's sum.  With DL_DPP_REDUCE the lane exchanges are DPP moves inside a 16-lane
+// row (mirror over 16 lanes, mirror over 8, then swaps of lane pairs of pairs and of lane
+// pairs), which need no LDS round trip; otherwise xor shuffles.  Callers reduce only where
+// every lane of the wave is active.
+#ifndef DL_DPP_REDUCE
+#define DL_DPP_REDUCE 1
+#endif
+template <int CTRL>
+__device__ __forceinline__ float dpp_move(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+template <int N>
+__device__ __forceinline__ float group_sum(float v) {
+  static_assert(N == 4 || N == 8 || N == 16, "DPP rows hold 16 lanes");
+  if constexpr (DL_DPP_REDUCE) {
+    if constexpr (N == 16) v += dpp_move<0x140>(v);   // row_mirror: lane i <- 15 - i
+    if constexpr (N >= 8) v += dpp_move<0x141>(v);    // row_half_mirror: lane i <- 7 - i
+    v += dpp_move<0x4E>(v);                           // quad_perm [2,3,0,1]
+    v += dpp_move<0xB1>(v);                           // quad_perm [1,0,3,2]
+  } else {
+#pragma unroll
+    for (int m = N / 2; m >= 1; m >>= 1) v += shfl_xor(v, m);
+  }
+  return v;
+}
+
 // Decay factors exp(x) for log-decay differences x <= 0: the hardware base-2
 // exponential of x * log2(e) (two instructions instead of the 13 of a correctly
 // rounded expf).  Its relative error is about 2^-24 * |x| * log2(e) plus one ulp
@@ -387,7 +414,7 @@ struct Cfg {
       return (rg + NRG * (j % q)) * LPE + j / q;
     }
   }
-  static_assert(LPE <= 64 && 64 % LPE == 0, "an entry's lanes share one wave");
+  static_assert(LPE <= 16 && 16 % LPE == 0, "an entry's lanes share one 16-lane row");
   static_assert(NT == threads_per_head(DK, DV), "launch bound must match the layout");
   static_assert(!(BONUS && DL == 1), "the bonus readout is only defined with per-key decay");
 };
@@ -622,8 +649,9 @@ void deltalog_kernel(KParams p) {
     // q.k (post-update readout of the new term) or r.(u*k) (RWKV6 bonus)
     float d = CF::BONUS ? qf * uf * kf : qf * kf;
     if (r0 >= DK) d = 0.f;                        // threads past dk hold a repeated row
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) d += shfl_xor(d, m);
+    d = group_sum<16>(d);
+    d += shfl_xor(d, 16);
+    d += shfl_xor(d, 32);
     if ((tid & 63) == 0) s_dotw[tid >> 6] = d;
   }
   __syncthreads();
@@ -684,11 +712,8 @@ void deltalog_kernel(KParams p) {
           s_kt[CF::kt_row_run(c_, x) * CF::KTS + e_] = 0.f;
         }
       }
-#pragma unroll
-      for (int m = CF::LPE / 2; m >= 1; m >>= 1) {
-        if constexpr (CF::NEEDS_C) ak += shfl_xor(ak, m);   // the delta-rule correction only
-        aq += shfl_xor(aq, m);
-      }
+      if constexpr (CF::NEEDS_C) ak = group_sum<CF::LPE>(ak);   // the delta-rule correction only
+      aq = group_sum<CF::LPE>(aq);
       if (c_ == 0 && i < L) {
         if constexpr (CF::NEEDS_C) s_gk[i] = ak;
         s_gq[i] = aq;
