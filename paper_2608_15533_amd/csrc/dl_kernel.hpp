@@ -88,8 +88,9 @@ __device__ __forceinline__ float shfl_xor(float v, int m) { return __shfl_xor(v,
 // Sum over aligned groups of N lanes (N = 4, 8 or 16), every lane of a group ending with
 // the group's sum.  With DL_DPP_REDUCE the lane exchanges are DPP moves inside a 16-lane
 // row (mirror over 16 lanes, mirror over 8, then swaps of lane pairs of pairs and of lane
-// pairs), which need no LDS round trip; otherwise xor shuffles.  Callers reduce only where
-// every lane of the wave is active.
+// pairs), and the exchanges across rows below are the gfx950 row-swap instructions:
+// none needs an LDS round trip.  Otherwise all are xor shuffles.  Callers reduce only
+// where every lane of the wave is active.
 #ifndef DL_DPP_REDUCE
 #define DL_DPP_REDUCE 1
 #endif
@@ -110,6 +111,31 @@ __device__ __forceinline__ float group_sum(float v) {
     for (int m = N / 2; m >= 1; m >>= 1) v += shfl_xor(v, m);
   }
   return v;
+}
+// v(lane) + v(lane ^ 16): v_permlane16_swap with both operands v hands each lane the two
+// values of its row pair.
+__device__ __forceinline__ float xor16_sum(float v) {
+  if constexpr (DL_DPP_REDUCE) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  } else {
+    return v + shfl_xor(v, 16);
+  }
+}
+// v(lane) + v(lane ^ 32), with v_permlane32_swap likewise.
+__device__ __forceinline__ float xor32_sum(float v) {
+  if constexpr (DL_DPP_REDUCE) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  } else {
+    return v + shfl_xor(v, 32);
+  }
+}
+__device__ __forceinline__ float4 xor16_sum(float4 v) {
+  return make_float4(xor16_sum(v.x), xor16_sum(v.y), xor16_sum(v.z), xor16_sum(v.w));
+}
+__device__ __forceinline__ float4 xor32_sum(float4 v) {
+  return make_float4(xor32_sum(v.x), xor32_sum(v.y), xor32_sum(v.z), xor32_sum(v.w));
 }
 
 // Decay factors exp(x) for log-decay differences x <= 0: the hardware base-2
@@ -649,9 +675,7 @@ void deltalog_kernel(KParams p) {
     // q.k (post-update readout of the new term) or r.(u*k) (RWKV6 bonus)
     float d = CF::BONUS ? qf * uf * kf : qf * kf;
     if (r0 >= DK) d = 0.f;                        // threads past dk hold a repeated row
-    d = group_sum<16>(d);
-    d += shfl_xor(d, 16);
-    d += shfl_xor(d, 32);
+    d = xor32_sum(xor16_sum(group_sum<16>(d)));
     if ((tid & 63) == 0) s_dotw[tid >> 6] = d;
   }
   __syncthreads();
@@ -755,15 +779,13 @@ void deltalog_kernel(KParams p) {
       }
     }
     // Rows of one column group live in lanes NCG apart inside a wave, then across waves.
-#pragma unroll
-    for (int m = NCG; m < 64; m <<= 1) {
-      if constexpr (CF::NEEDS_C) {
-        cv.x += shfl_xor(cv.x, m); cv.y += shfl_xor(cv.y, m);
-        cv.z += shfl_xor(cv.z, m); cv.w += shfl_xor(cv.w, m);
-      }
-      ov.x += shfl_xor(ov.x, m); ov.y += shfl_xor(ov.y, m);
-      ov.z += shfl_xor(ov.z, m); ov.w += shfl_xor(ov.w, m);
+    static_assert(NCG == 16 || NCG == 32, "column groups fill one or two 16-lane rows");
+    if constexpr (NCG == 16) {
+      if constexpr (CF::NEEDS_C) cv = xor16_sum(cv);
+      ov = xor16_sum(ov);
     }
+    if constexpr (CF::NEEDS_C) cv = xor32_sum(cv);
+    ov = xor32_sum(ov);
     if constexpr (CF::NW > 1) {
       const int w = tid / 64, lane = tid % 64;
       if (lane < NCG) {
