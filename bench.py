@@ -145,10 +145,26 @@ def code_only(text):
     return " ".join("".join(out).split())
 
 
-def kernel_source_hash():
+def library_build_flags():
+    """The compiler flags the library in use was built with (dl_build_flags()), read with
+    a bare ctypes load so that no GPU runtime state is touched; the flags a default build
+    would use when no library is built."""
+    import ctypes
+    from paper_2608_15533_amd import build as B
+    path = os.environ.get("DELTALOG_LIB") or B.LIB
+    try:
+        lib = ctypes.CDLL(path)
+        lib.dl_build_flags.restype = ctypes.c_char_p
+        return lib.dl_build_flags().decode()
+    except (OSError, AttributeError):
+        return B.build_flags_string()
+
+
+def kernel_source_hash(build_flags=None):
     """sha256 over the code of the kernel sources and the public header, comments and
-    layout excluded: any change to the code invalidates counter figures taken earlier,
-    an edit of a comment does not."""
+    layout excluded, and over the compiler flags of the build (``build_flags``; default:
+    those of the library in use): any change to the code or to the flags invalidates
+    counter figures taken earlier, an edit of a comment does not."""
     files = sorted(glob.glob(os.path.join(ROOT, "paper_2608_15533_amd", "csrc", "*")))
     files.append(os.path.join(ROOT, "include", "deltalog.h"))
     h = hashlib.sha256()
@@ -156,6 +172,8 @@ def kernel_source_hash():
         h.update(os.path.basename(f).encode())
         with open(f, encoding="utf-8", errors="surrogateescape") as fh:
             h.update(code_only(fh.read()).encode("utf-8", errors="surrogateescape"))
+    flags = library_build_flags() if build_flags is None else build_flags
+    h.update(b"flags:" + " ".join(flags.split()).encode())
     return h.hexdigest()[:16]
 
 

@@ -40,8 +40,9 @@
  *    device can see (a slot id outside [0, B), a live length outside [0, C]) makes the
  *    affected (slot, head) skip its work and ORs a code into *state->err (if non-NULL):
  *    1 = bad slot id, 2 = live length out of range.
- *  - Alignment: S, k_log, u_log, q, k, v and o must be 16-byte aligned; the other
- *    float/int32 arrays 4-byte aligned.
+ *  - Alignment: S, k_log, u_log, q, k, v and o must be 16-byte aligned, and so must
+ *    lam_log when dl == dk (KDA, RWKV6, GLA: its rows are read 16 bytes at a time);
+ *    the other float/int32 arrays 4-byte aligned.
  *  - Supported shapes: dk, dv in {64, 128}; 1 <= M <= 64.
  */
 #ifndef DELTALOG_H
@@ -117,6 +118,7 @@ typedef struct {
   void*    k_log;    /* [B,H,C,dk]  in_dtype   key-side factors   (may be NULL if C == 0) */
   void*    u_log;    /* [B,H,C,dv]  u_log_dtype value-side factors (may be NULL if C == 0)*/
   float*   lam_log;  /* [B,H,C,dl]  fp32 snapshot of ell per entry (may be NULL if C == 0)*/
+                     /*             16-byte aligned when dl == dk, else 4-byte            */
                      /*             for dl == 1 stored entry-major, [B,C,H]               */
                      /*             (ignored, may be NULL, for LINATTN)                  */
   int32_t* len;      /* [B,H]       live-log length L in [0, C]                          */
@@ -195,6 +197,11 @@ const char* dl_status_str(int status);
 
 /* DL_ABI_VERSION of the loaded library. */
 int dl_abi_version(void);
+
+/* The compiler flags the library's kernels were built with beyond the optimisation
+ * level and target (static storage), so that measurements can be matched to the exact
+ * build that produced them. */
+const char* dl_build_flags(void);
 
 #ifdef __cplusplus
 }

@@ -15,8 +15,12 @@ Contents
                    and the equivalence argument of Sec. 3.2 ("Closure under the recurrence").
 
 All arithmetic is float64; inputs are upcast from the exact bytes the GPU consumes.
-Every function is pinned by ``tests/test_oracle_pins.py`` (closed forms, special cases,
-2x2 brute force in exact rationals, invariants); nothing here is "parity unpinned".
+Every public function is exercised by ``tests/test_oracle_pins.py`` against something
+other than itself (closed forms, special cases, 2x2 brute force in exact rationals,
+invariants, a plain GEMM), and ``tests/test_oracle_mutants.py`` shows that a planted
+mistake in any term fails one of those pins.  The pinned functions are: ``eager.row_decay``,
+``eager.gdn_kda_step``, ``eager.rwkv6_step``, ``eager.additive_step``, ``eager.eager_step``,
+``eager.rel_fro`` and every method of ``deltalog_model.DeltaLogModel``.
 """
 
 from . import eager, deltalog_model  # noqa: F401

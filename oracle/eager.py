@@ -137,23 +137,6 @@ def eager_step(op, S, q, k, v, beta, lam, u=None, correction="decayed"):
     raise ValueError(op)
 
 
-def eager_rollout(op, S0, steps, u=None, keep_states=False):
-    """Run the eager recurrence over a sequence of step inputs.
-
-    ``steps`` is an iterable of dicts with keys q, k, v, beta, lam (beta used by the
-    delta rule only; lam may be None for linear attention).  Returns (outputs
-    [T, ..., dv], final state, states or None).
-    """
-    S = _f64(S0)
-    outs, states = [], []
-    for st in steps:
-        S, o = eager_step(op, S, st["q"], st["k"], st["v"], st.get("beta"), st.get("lam"), u=u)
-        outs.append(o)
-        if keep_states:
-            states.append(S.copy())
-    return np.stack(outs), S, (states if keep_states else None)
-
-
 def rel_fro(x, ref):
     """Relative Frobenius error ||x - ref|| / ||ref|| in float64 (the parity metric)."""
     x, ref = _f64(x), _f64(ref)

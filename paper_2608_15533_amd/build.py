@@ -32,10 +32,18 @@ def hipcc():
     return os.path.join(rocm, "bin", "hipcc")
 
 
+def build_flags_string(extra=()):
+    """The compiler flags that shape the kernels (the fixed device flags and any extra
+    ones, e.g. -D tuning macros), as the library reports them through dl_build_flags()."""
+    return " ".join([*DEVICE_FLAGS, *extra])
+
+
 def _compile(src, extra):
     obj = os.path.join(BUILD_DIR, os.path.basename(src) + ".o")
+    flags_def = '-DDL_BUILD_FLAGS="' + build_flags_string(extra).replace('"', "'") + '"'
     cmd = [hipcc(), "-c", "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
-           "-I", INCLUDE, "-I", CSRC, *DEVICE_FLAGS, *extra, os.path.join(CSRC, src), "-o", obj]
+           "-I", INCLUDE, "-I", CSRC, *DEVICE_FLAGS, *extra, flags_def,
+           os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{' '.join(cmd)}\n{r.stdout}\n{r.stderr}")

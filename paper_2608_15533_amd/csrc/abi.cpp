@@ -18,6 +18,7 @@ bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p
 
 bool is_delta(int op) { return op == DL_OP_GDN || op == DL_OP_KDA; }
 bool has_decay(int op) { return op != DL_OP_LINATTN; }
+bool per_key(int op) { return op == DL_OP_KDA || op == DL_OP_RWKV6 || op == DL_OP_GLA; }
 
 int check_desc(const dl_desc* d) {
   if (!d) return DL_E_NULL;
@@ -72,7 +73,8 @@ int check_state(const dl_desc* d, const dl_state* s) {
   if (!aligned(s->S, 16) || !aligned(s->len, 4)) return DL_E_ALIGN;
   if (s->k_log && !aligned(s->k_log, 16)) return DL_E_ALIGN;
   if (s->u_log && !aligned(s->u_log, 16)) return DL_E_ALIGN;
-  if (s->lam_log && !aligned(s->lam_log, 4)) return DL_E_ALIGN;
+  // Per-key snapshot rows are read with 16-byte loads.
+  if (s->lam_log && !aligned(s->lam_log, per_key(d->op) ? 16 : 4)) return DL_E_ALIGN;
   if (s->err && !aligned(s->err, 4)) return DL_E_ALIGN;
   return DL_OK;
 }
@@ -132,6 +134,11 @@ int launch(const dl_desc* d, int mode, const KParams& p, hipStream_t stream) {
 extern "C" {
 
 int dl_abi_version(void) { return DL_ABI_VERSION; }
+
+#ifndef DL_BUILD_FLAGS
+#define DL_BUILD_FLAGS ""
+#endif
+const char* dl_build_flags(void) { return DL_BUILD_FLAGS; }
 
 const char* dl_status_str(int status) {
   switch (status) {

@@ -42,7 +42,7 @@ TORCH_DTYPES = {"f32": torch.float32, "bf16": torch.bfloat16}
 
 EXPORTED = ("dl_eager_step", "dl_append_step", "dl_merge", "dl_readout",
             "dl_append_step_tiled", "dl_tiled_workspace_bytes", "dl_status_str",
-            "dl_abi_version")
+            "dl_abi_version", "dl_build_flags")
 
 
 class dl_desc(ctypes.Structure):
@@ -83,6 +83,8 @@ for _f in ("dl_eager_step", "dl_append_step", "dl_merge", "dl_readout", "dl_appe
     getattr(_lib, _f).restype = ctypes.c_int
 _lib.dl_status_str.argtypes = [ctypes.c_int]
 _lib.dl_status_str.restype = ctypes.c_char_p
+_lib.dl_build_flags.argtypes = []
+_lib.dl_build_flags.restype = ctypes.c_char_p
 
 lib = _lib
 
@@ -99,6 +101,10 @@ def dl_status_str(status):
 
 def dl_abi_version():
     return _lib.dl_abi_version()
+
+
+def dl_build_flags():
+    return _lib.dl_build_flags().decode()
 
 
 if dl_abi_version() != DL_ABI_VERSION:
@@ -218,10 +224,16 @@ def _stream(stream):
 
 
 def _rows(desc, slots, n):
+    """(device slot-list pointer or None, rows n of the launch).  Token row i drives slot
+    slots[i] for i < n, so a token given with the call must hold at least n rows (extra
+    rows are not read); without a slot list n is the token's row count or B."""
+    rows = (desc.num_slots if n is None else n) if slots is None else slots.numel()
+    if n is not None and n < rows:
+        raise ValueError(f"the token holds {n} rows but the launch drives {rows}")
     if slots is None:
-        return None, desc.num_slots if n is None else n
-    _need(slots, "slots", torch.int32, (slots.numel(),))
-    return slots.data_ptr(), slots.numel()
+        return None, rows
+    _need(slots, "slots", torch.int32, (rows,))
+    return slots.data_ptr(), rows
 
 
 def _check(rc, where):

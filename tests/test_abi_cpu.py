@@ -10,12 +10,19 @@ import re
 import subprocess
 
 import pytest
+import torch
 
 from paper_2608_15533_amd import deltalog as D
 
 HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "deltalog.h")
 
 A = 0x10000000          # a fake, 256-byte aligned "device" address
+
+# These calls hand fake device addresses to the real library and rely on its host-side
+# checks to refuse every one of them; where a GPU is visible a regression in those checks
+# would launch a kernel on such an address, so the module runs only where none is.
+pytestmark = pytest.mark.skipif(torch.cuda.device_count() > 0,
+                                reason="fake device addresses: only on a host without a GPU")
 
 
 def _declared_functions():
@@ -190,6 +197,27 @@ def test_alignment(where, field, off):
         t = token()
         setattr(t, field, getattr(t, field) + off)
         assert append(desc(), t=t) == D.DL_E_ALIGN
+
+
+@pytest.mark.parametrize("op,off,code", [
+    ("kda", 4, D.DL_E_ALIGN), ("rwkv6", 8, D.DL_E_ALIGN), ("gla", 12, D.DL_E_ALIGN),
+    ("gdn", 4, D.DL_E_ALIGN + 100), ("retnet", 8, D.DL_E_ALIGN + 100),
+])
+def test_per_key_snapshots_need_16_byte_alignment(op, off, code):
+    """Per-key Lam_log rows are read 16 bytes at a time: lam_log must be 16-byte aligned
+    for KDA, RWKV6 and GLA; one snapshot per head (GDN, RetNet) needs 4 bytes.  (+100
+    marks the calls that pass the state checks and stop at the misaligned output.)"""
+    dk = 64 if op == "rwkv6" else 128
+    d = D.make_desc(op, 4, 2, dk, dk, 16, "bf16")
+    t = token(beta=None if op not in ("gdn", "kda") else A + 0x900000,
+              u=A + 0xC00000 if op == "rwkv6" else None)
+    s = state()
+    s.lam_log += off
+    if code == D.DL_E_ALIGN:
+        assert append(d, s=s, t=t) == D.DL_E_ALIGN
+    else:
+        assert append(d, s=s, t=t, o=A + 4) == D.DL_E_ALIGN   # stopped at o, not at lam_log
+        assert append(d, s=s, t=t, o=None) == D.DL_E_NULL
 
 
 def test_output_checks():

@@ -10,10 +10,17 @@ import ctypes
 import random
 
 import pytest
+import torch
 
 from paper_2608_15533_amd import deltalog as D
 
 A = 0x10000000
+
+# These calls hand fake device addresses to the real library and rely on its host-side
+# checks to refuse every one of them; where a GPU is visible a regression in those checks
+# would launch a kernel on such an address, so the module runs only where none is.
+pytestmark = pytest.mark.skipif(torch.cuda.device_count() > 0,
+                                reason="fake device addresses: only on a host without a GPU")
 O_BAD = A + 0xB00004                                  # misaligned output: never launches
 
 

@@ -93,3 +93,17 @@ def test_kernel_hash_ignores_comments_but_not_code(monkeypatch, tmp_path):
     assert bench.kernel_source_hash() == h0
     f.write_text(text.replace("#pragma once", "#pragma once\nstatic int dl_changed = 1;", 1))
     assert bench.kernel_source_hash() != h0
+
+
+def test_kernel_hash_covers_the_build_flags():
+    """A library built with other flags (e.g. a -D tuning macro) hashes differently, so a
+    counter profile taken on one build is never attached to another."""
+    from paper_2608_15533_amd import build as B
+    h0 = bench.kernel_source_hash(B.build_flags_string())
+    assert bench.kernel_source_hash(B.build_flags_string(["-DDL_XCD_CHUNK=16"])) != h0
+    assert bench.kernel_source_hash(" ".join(B.DEVICE_FLAGS) + "  ") == h0   # layout only
+
+
+def test_library_reports_the_flags_it_was_built_with():
+    from paper_2608_15533_amd import build as B
+    assert bench.library_build_flags() == B.build_flags_string()
