@@ -67,7 +67,8 @@ typedef enum {
   DL_E_ALIGN = -4,       /* pointer not aligned as required                             */
   DL_E_UNSUPPORTED = -5, /* dk/dv/M/op outside the supported set                        */
   DL_E_HIP = -6,         /* the kernel launch failed                                    */
-  DL_E_VERSION = -7      /* desc->abi_version != DL_ABI_VERSION                         */
+  DL_E_VERSION = -7,     /* desc->abi_version != DL_ABI_VERSION                         */
+  DL_E_SCRATCH = -8      /* needs more than DL_NOALLOC_SCRATCH_BYTES of scratch          */
 } dl_status;
 
 typedef enum {
@@ -191,6 +192,29 @@ int dl_append_step_tiled(const dl_desc* desc, const dl_state* state, const dl_to
 /* Bytes of workspace dl_append_step_tiled needs for n rows with split replay:
  * n * H * 2 * (M - 1) * sizeof(float) (0 when M == 1).  Writes *bytes. */
 int dl_tiled_workspace_bytes(const dl_desc* desc, int32_t n, size_t* bytes);
+
+/* Size of the fixed scratch of dl_append_step_tiled_noalloc, per GPU. */
+#define DL_NOALLOC_SCRATCH_BYTES (4u << 20)
+
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): dl_append_step_tiled with split
+ * replay, its workspace taken from a scratch array of DL_NOALLOC_SCRATCH_BYTES that the
+ * library holds in device memory, one per GPU, for the life of the process.  The caller
+ * still passes the state, token and output buffers; the call allocates and frees
+ * nothing and enqueues exactly the launches of dl_append_step_tiled(..., split_replay=1,
+ * ...).
+ * The scratch needed is dl_tiled_workspace_bytes(desc, n); a call that needs more than
+ * DL_NOALLOC_SCRATCH_BYTES returns DL_E_SCRATCH (after the argument checks, before any
+ * HIP call) and enqueues nothing.
+ * Every call on a GPU shares that GPU's scratch: calls that may overlap on one GPU (on
+ * different streams, or from different threads without ordering) race and must not be
+ * issued; calls ordered on one stream are safe.  The scratch keeps the last call's
+ * contents; a call reads only what it wrote itself.  On its first call on a device the
+ * entry point looks up that device's scratch address (a HIP runtime query, no
+ * allocation) and keeps it; a failed lookup returns DL_E_HIP. */
+int dl_append_step_tiled_noalloc(const dl_desc* desc, const dl_state* state,
+                                 const dl_token* tok, float* o, const int32_t* slots,
+                                 int32_t n, int32_t value_tiles, hipStream_t stream);
 
 /* Human-readable name of a dl_status value (static storage). */
 const char* dl_status_str(int status);

@@ -22,7 +22,7 @@ LIB = os.path.join(PKG, "libdeltalog.so")
 ARCH = "gfx950"
 
 SOURCES = ["abi.cpp", "dl_gdn.hip", "dl_kda.hip", "dl_rwkv6.hip", "dl_linattn.hip",
-           "dl_retnet.hip", "dl_gla.hip"]
+           "dl_retnet.hip", "dl_gla.hip", "dl_noalloc.hip"]
 
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 

@@ -131,6 +131,46 @@ int launch(const dl_desc* d, int mode, const KParams& p, hipStream_t stream) {
 
 }  // namespace
 
+namespace dl {
+
+int tiled_check(const dl_desc* desc, const dl_state* state, const dl_token* tok, float* o,
+                const int32_t* slots, int32_t n, int32_t value_tiles) {
+  DL_TRY(check_desc(desc));
+  DL_TRY(check_rows(desc, slots, n));
+  if (value_tiles != 2 && value_tiles != 4) return DL_E_UNSUPPORTED;
+  if (desc->state_dtype != DL_F32) return DL_E_DTYPE;
+  if (n == 0) return DL_OK;               // nothing to do, whatever the other pointers are
+  if (int64_t(n) * desc->heads * value_tiles > int64_t(0x7fffffff)) return DL_E_SHAPE;
+  DL_TRY(check_state(desc, state));
+  DL_TRY(check_token(desc, tok));
+  if (!o) return DL_E_NULL;
+  if (!aligned(o, 16)) return DL_E_ALIGN;
+  return DL_OK;
+}
+
+int tiled_launch(const dl_desc* desc, const dl_state* state, const dl_token* tok, float* o,
+                 const int32_t* slots, int32_t n, int32_t value_tiles, bool split, float* coef,
+                 hipStream_t stream) {
+  KParams p = base_params(desc, slots, n);
+  set_state(p, state);
+  set_token(p, tok);
+  p.o = o;
+  const bool bf16 = desc->in_dtype == DL_BF16;
+  if (!split) coef = nullptr;
+  hipError_t e = hipErrorInvalidValue;
+  switch (desc->op) {
+    case DL_OP_GDN: e = launch_tiled_gdn(desc->dk, desc->dv, bf16, value_tiles, split, p, coef, stream); break;
+    case DL_OP_KDA: e = launch_tiled_kda(desc->dk, desc->dv, bf16, value_tiles, split, p, coef, stream); break;
+    case DL_OP_RWKV6: e = launch_tiled_rwkv6(desc->dk, desc->dv, bf16, value_tiles, split, p, coef, stream); break;
+    case DL_OP_LINATTN: e = launch_tiled_linattn(desc->dk, desc->dv, bf16, value_tiles, split, p, coef, stream); break;
+    case DL_OP_RETNET: e = launch_tiled_retnet(desc->dk, desc->dv, bf16, value_tiles, split, p, coef, stream); break;
+    case DL_OP_GLA: e = launch_tiled_gla(desc->dk, desc->dv, bf16, value_tiles, split, p, coef, stream); break;
+  }
+  return e == hipSuccess ? DL_OK : DL_E_HIP;
+}
+
+}  // namespace dl
+
 extern "C" {
 
 int dl_abi_version(void) { return DL_ABI_VERSION; }
@@ -150,6 +190,7 @@ const char* dl_status_str(int status) {
     case DL_E_UNSUPPORTED: return "DL_E_UNSUPPORTED: dk, dv, merge interval or operator not supported";
     case DL_E_HIP: return "DL_E_HIP: kernel launch failed";
     case DL_E_VERSION: return "DL_E_VERSION: descriptor ABI version mismatch";
+    case DL_E_SCRATCH: return "DL_E_SCRATCH: the call needs more than the allocation-free entry point's fixed scratch";
   }
   return "unknown dl_status";
 }
@@ -231,16 +272,8 @@ int dl_append_step_tiled(const dl_desc* desc, const dl_state* state, const dl_to
                          float* o, const int32_t* slots, int32_t n, int32_t value_tiles,
                          int32_t split_replay, void* workspace, size_t workspace_bytes,
                          hipStream_t stream) {
-  DL_TRY(check_desc(desc));
-  DL_TRY(check_rows(desc, slots, n));
-  if (value_tiles != 2 && value_tiles != 4) return DL_E_UNSUPPORTED;
-  if (desc->state_dtype != DL_F32) return DL_E_DTYPE;
+  DL_TRY(dl::tiled_check(desc, state, tok, o, slots, n, value_tiles));
   if (n == 0) return DL_OK;               // nothing to do, whatever the other pointers are
-  if (int64_t(n) * desc->heads * value_tiles > int64_t(0x7fffffff)) return DL_E_SHAPE;
-  DL_TRY(check_state(desc, state));
-  DL_TRY(check_token(desc, tok));
-  if (!o) return DL_E_NULL;
-  if (!aligned(o, 16)) return DL_E_ALIGN;
   const bool split = split_replay != 0;
   if (split && desc->merge_interval > 1) {
     size_t need = 0;
@@ -249,22 +282,8 @@ int dl_append_step_tiled(const dl_desc* desc, const dl_state* state, const dl_to
     if (!aligned(workspace, 16)) return DL_E_ALIGN;
     if (workspace_bytes < need) return DL_E_SHAPE;
   }
-  KParams p = base_params(desc, slots, n);
-  set_state(p, state);
-  set_token(p, tok);
-  p.o = o;
-  const bool bf16 = desc->in_dtype == DL_BF16;
-  float* coef = split ? static_cast<float*>(workspace) : nullptr;
-  hipError_t e = hipErrorInvalidValue;
-  switch (desc->op) {
-    case DL_OP_GDN: e = dl::launch_tiled_gdn(desc->dk, desc->dv, bf16, value_tiles, split, p, coef, stream); break;
-    case DL_OP_KDA: e = dl::launch_tiled_kda(desc->dk, desc->dv, bf16, value_tiles, split, p, coef, stream); break;
-    case DL_OP_RWKV6: e = dl::launch_tiled_rwkv6(desc->dk, desc->dv, bf16, value_tiles, split, p, coef, stream); break;
-    case DL_OP_LINATTN: e = dl::launch_tiled_linattn(desc->dk, desc->dv, bf16, value_tiles, split, p, coef, stream); break;
-    case DL_OP_RETNET: e = dl::launch_tiled_retnet(desc->dk, desc->dv, bf16, value_tiles, split, p, coef, stream); break;
-    case DL_OP_GLA: e = dl::launch_tiled_gla(desc->dk, desc->dv, bf16, value_tiles, split, p, coef, stream); break;
-  }
-  return e == hipSuccess ? DL_OK : DL_E_HIP;
+  return dl::tiled_launch(desc, state, tok, o, slots, n, value_tiles, split,
+                          static_cast<float*>(workspace), stream);
 }
 
 }  // extern "C"

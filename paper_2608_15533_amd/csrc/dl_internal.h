@@ -65,4 +65,12 @@ DL_DECLARE_TILED(retnet);
 DL_DECLARE_TILED(gla);
 #undef DL_DECLARE_TILED
 
+// The argument checks of the value-tiled step other than its workspace (host only; no
+// HIP call), and its launches with `coef` as the split-replay scratch.
+int tiled_check(const dl_desc* desc, const dl_state* state, const dl_token* tok, float* o,
+                const int32_t* slots, int32_t n, int32_t value_tiles);
+int tiled_launch(const dl_desc* desc, const dl_state* state, const dl_token* tok, float* o,
+                 const int32_t* slots, int32_t n, int32_t value_tiles, bool split, float* coef,
+                 hipStream_t stream);
+
 }  // namespace dl

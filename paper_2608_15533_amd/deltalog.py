@@ -31,6 +31,8 @@ DL_ABI_VERSION = 4
 DL_MAX_MERGE_INTERVAL = 64
 DL_OK, DL_E_NULL, DL_E_SHAPE, DL_E_DTYPE, DL_E_ALIGN, DL_E_UNSUPPORTED, DL_E_HIP, DL_E_VERSION = (
     0, -1, -2, -3, -4, -5, -6, -7)
+DL_E_SCRATCH = -8
+DL_NOALLOC_SCRATCH_BYTES = 4 << 20
 DL_OP_GDN, DL_OP_KDA, DL_OP_RWKV6, DL_OP_LINATTN, DL_OP_RETNET, DL_OP_GLA = 0, 1, 2, 3, 4, 5
 DL_F32, DL_BF16 = 0, 1
 OP_IDS = {"gdn": DL_OP_GDN, "kda": DL_OP_KDA, "rwkv6": DL_OP_RWKV6, "linattn": DL_OP_LINATTN,
@@ -42,7 +44,7 @@ TORCH_DTYPES = {"f32": torch.float32, "bf16": torch.bfloat16}
 
 EXPORTED = ("dl_eager_step", "dl_append_step", "dl_merge", "dl_readout",
             "dl_append_step_tiled", "dl_tiled_workspace_bytes", "dl_status_str",
-            "dl_abi_version", "dl_build_flags")
+            "dl_abi_version", "dl_build_flags", "dl_append_step_tiled_noalloc")
 
 
 class dl_desc(ctypes.Structure):
@@ -78,8 +80,11 @@ _lib.dl_append_step_tiled.argtypes = [ctypes.POINTER(dl_desc), ctypes.POINTER(dl
                                       ctypes.c_int32, ctypes.c_int32, _P, ctypes.c_size_t, _P]
 _lib.dl_tiled_workspace_bytes.argtypes = [ctypes.POINTER(dl_desc), ctypes.c_int32,
                                           ctypes.POINTER(ctypes.c_size_t)]
+_lib.dl_append_step_tiled_noalloc.argtypes = [ctypes.POINTER(dl_desc), ctypes.POINTER(dl_state),
+                                              ctypes.POINTER(dl_token), _P, _P, ctypes.c_int32,
+                                              ctypes.c_int32, _P]
 for _f in ("dl_eager_step", "dl_append_step", "dl_merge", "dl_readout", "dl_append_step_tiled",
-           "dl_tiled_workspace_bytes", "dl_abi_version"):
+           "dl_tiled_workspace_bytes", "dl_abi_version", "dl_append_step_tiled_noalloc"):
     getattr(_lib, _f).restype = ctypes.c_int
 _lib.dl_status_str.argtypes = [ctypes.c_int]
 _lib.dl_status_str.restype = ctypes.c_char_p
@@ -309,3 +314,15 @@ def dl_append_step_tiled(desc, state, tok, o, slots=None, value_tiles=4, split_r
                                      ctypes.byref(tok.struct), _ptr(o), sp, n,
                                      int(value_tiles), int(bool(split_replay)), wp, wn,
                                      _stream(stream)), "dl_append_step_tiled")
+
+
+def dl_append_step_tiled_noalloc(desc, state, tok, o, slots=None, value_tiles=4, stream=None):
+    """dl_append_step_tiled with split replay whose coefficient scratch is the library's
+    fixed per-GPU array (DL_NOALLOC_SCRATCH_BYTES): the call allocates nothing.  Calls
+    that may overlap on one GPU race on that array."""
+    sp, n = _rows(desc, slots, tok.n)
+    _need(o, "o", torch.float32, (n, desc.heads, desc.dv))
+    _check(_lib.dl_append_step_tiled_noalloc(ctypes.byref(desc), ctypes.byref(state.struct),
+                                             ctypes.byref(tok.struct), _ptr(o), sp, n,
+                                             int(value_tiles), _stream(stream)),
+           "dl_append_step_tiled_noalloc")

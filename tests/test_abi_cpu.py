@@ -44,7 +44,7 @@ def test_header_functions_are_exported():
 
 def test_version_and_status_strings():
     assert D.dl_abi_version() == D.DL_ABI_VERSION == 4
-    for code in range(0, -8, -1):
+    for code in range(0, -9, -1):
         s = D.dl_status_str(code)
         assert s.startswith("DL_") and s != "unknown dl_status"
     assert D.dl_status_str(-99) == "unknown dl_status"
@@ -291,3 +291,38 @@ def test_binding_refuses_to_load_without_the_library(tmp_path):
                            capture_output=True, text=True, timeout=300)
         assert r.returncode != 0, mod
         assert "ImportError" in r.stderr and "no non-HIP fallback" in r.stderr, r.stderr[-400:]
+
+
+def noalloc(d, s=None, t=None, o=A + 0xB00000, slots=None, n=4, nv=4):
+    return D.lib.dl_append_step_tiled_noalloc(ctypes.byref(d), ctypes.byref(s or state()),
+                                              ctypes.byref(t or token()), o, slots, n, nv, None)
+
+
+def test_noalloc_rejections_before_any_hip_call():
+    """The allocation-free entry point runs the tiled step's checks first (misaligned
+    output last), then refuses a call whose coefficient scratch would exceed the fixed
+    array, all before its first HIP call (the scratch lookup)."""
+    assert noalloc(desc(), o=A + 4) == D.DL_E_ALIGN
+    assert noalloc(desc(), nv=3) == D.DL_E_UNSUPPORTED
+    assert noalloc(desc(state_dtype=D.DL_BF16)) == D.DL_E_DTYPE
+    assert noalloc(desc(), s=state(len=None)) == D.DL_E_NULL
+    assert noalloc(desc(), t=token(beta=None)) == D.DL_E_NULL
+    assert noalloc(desc(), n=0) == D.DL_OK
+    assert noalloc(desc(), n=5) == D.DL_E_SHAPE
+    # n * H * 2 * (M - 1) * 4 bytes: 2048 x 32 heads at M = 64 needs 31.5 MiB
+    big = D.make_desc("gdn", 2048, 32, 128, 128, 64, "bf16")
+    assert D.dl_tiled_workspace_bytes(big, 2048) > D.DL_NOALLOC_SCRATCH_BYTES
+    assert noalloc(big, n=2048) == D.DL_E_SCRATCH
+    # the largest row count that fits is accepted by the size check
+    fit = D.DL_NOALLOC_SCRATCH_BYTES // (32 * 2 * 63 * 4)
+    assert D.dl_tiled_workspace_bytes(big, fit) <= D.DL_NOALLOC_SCRATCH_BYTES
+    assert D.dl_tiled_workspace_bytes(big, fit + 1) > D.DL_NOALLOC_SCRATCH_BYTES
+    assert noalloc(big, n=fit + 1, slots=A) == D.DL_E_SCRATCH
+    assert "scratch" in D.dl_status_str(D.DL_E_SCRATCH)
+
+
+def test_noalloc_scratch_size_matches_the_header():
+    text = open(HEADER).read()
+    assert "#define DL_NOALLOC_SCRATCH_BYTES (4u << 20)" in text
+    assert D.DL_NOALLOC_SCRATCH_BYTES == 4 << 20
+
