@@ -2,19 +2,28 @@
 
     python bench.py [--workload NAME] [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
 
-Default workload: GDN delta-rule decode, 64 sequences x 32 heads, dk = dv = 128, fp32
-state, bf16 q/k/v, merge interval M = 16.  R = 8 independent copies of that layer's
-state (1.2 GiB in all) are stepped in turn, like consecutive layers of a model, so the
-working set is far larger than the 256 MB last-level cache and every step streams its
-state from HBM.  A step is one decode token through all R layer states (R launches of
-dl_append_step); the reported value is per-layer token-updates per second,
-B * R * K / elapsed.  Other workloads (--workload): KDA 128x32x128^2 at M in {8,16,32}
-(R = 4), RWKV6 128x40x64^2 at M = 16 (R = 12), and the 24-layer GDN stack of 256
-sequences with staggered log fill (R = 24 layers; value = 256 * K / elapsed).
+Default workload: the serving-step stack -- 24 GDN delta-rule layers, each 256
+sequences x 32 heads, dk = dv = 128, fp32 state, bf16 q/k/v, merge interval M = 16, with
+per-sequence log fill offsets uniform in [0, M) so that merges are staggered across
+sequences (every launch mixes appending and merging slots).  A step is one decode token
+of all 256 sequences through all 24 layers (24 launches of dl_append_step); the value is
+sequence tokens per second, 256 * K / elapsed.  Other workloads (--workload): GDN
+64x32x128^2 at M = 16 (R = 8 layer states), KDA 128x32x128^2 at M in {8,16,32} (R = 4),
+RWKV6 128x40x64^2 at M = 16 (R = 12), linear attention, RetNet, GLA, and the small GDN
+latency case 1x2x64^2 at M = 8 (fp32 or bf16 q/k/v).  Single-layer workloads step R
+independent copies of the layer's state in turn, like consecutive layers of a model, so
+the working set is far larger than the 256 MB last-level cache; their value is per-layer
+token-updates per second, B * R * K / elapsed.
 
 Token inputs come from a pool of 16 seeded steps of the workload generator, cycled over
 the run; initial states are drawn on the device (seeded torch normal, std 0.02).  The
 values do not change the cost of any kernel.
+
+Timing: W untimed steps, then --repeats timed rollouts of exactly K steps each, every one
+bracketed by torch.cuda.synchronize() and HIP events on the launch stream (the state
+keeps decoding from one rollout to the next; K is a multiple of M, so every rollout has
+the same phase mix); the value is the median rollout.  The same K steps are also timed
+as replays of one captured HIP graph (or as direct launches, under --graph).
 
 Besides the contract fields the JSON line carries: the eager dense baseline
 (dl_eager_step on the same states), the per-phase split (append at each live length,
@@ -22,7 +31,8 @@ merge; a separate pass with an event pair around each step's launches), the roof
 the dominant kernel (algorithmic bytes of the average launch over its average duration,
 the duration taken from HIP events around the timed region on the launch stream), the
 HBM traffic of that kernel from the committed counter profile when the kernel sources
-still match it, and the fp64 CPU oracle timed on a bounded sample on this host.
+and build flags still match it, and the fp64 CPU oracle timed on a bounded sample on this
+host, on all its cores and on one.
 """
 
 import argparse
@@ -48,6 +58,9 @@ POOL = 16
 def workloads():
     from paper_2608_15533_amd import workloads as W
     return {
+        "gdn_b1_h2_d64_m8": (W.GDN_SMALL, 1),
+        "gdn_b1_h2_d64_m8_bf16": (W.GDN_SMALL.with_(name="gdn_b1_h2_d64_m8_bf16",
+                                                    in_dtype="bf16"), 1),
         "gdn_b64_h32_d128_m16": (W.GDN_B64, 8),
         "kda_b128_h32_d128_m8": (W.kda_with_merge_interval(8), 4),
         "kda_b128_h32_d128_m16": (W.kda_with_merge_interval(16), 4),
@@ -63,9 +76,13 @@ def workloads():
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--workload", default="gdn_b64_h32_d128_m16", choices=sorted(workloads()))
-    ap.add_argument("--steps", type=int, default=256)
+    ap.add_argument("--workload", default="gdn_stack24_b256_h32_d128_m16",
+                    choices=sorted(workloads()))
+    ap.add_argument("--steps", type=int, default=0,
+                    help="timed steps per rollout (0: the workload's own decode length)")
     ap.add_argument("--warmup", type=int, default=32)
+    ap.add_argument("--repeats", type=int, default=5,
+                    help="timed rollouts of --steps steps; the value is their median")
     ap.add_argument("--replicas", type=int, default=0, help="layer states (0: workload default)")
     ap.add_argument("--merge-interval", type=int, default=0,
                     help="override the workload's merge interval M (0: workload default)")
@@ -82,15 +99,25 @@ def parse():
     ap.add_argument("--graph", action="store_true",
                     help="submit the timed steps as replays of one HIP graph holding 16 steps "
                          "x R launches (the same launches, captured once)")
+    ap.add_argument("--single-submission", action="store_true",
+                    help="time only the chosen submission (direct launches, or --graph), "
+                         "not the other one as well (counter runs)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="time budget of each of the two CPU oracle runs (all cores, one core)")
     ap.add_argument("--decode-loop", default="", metavar="MODES",
                     help="instead of the kernel bench: time the decode loop (slot allocator, "
                          "graph-captured steps) under comma-separated scheduling modes "
                          "(fused, phased, phased_concurrent; 'all'), with and without graphs")
     ap.add_argument("--layers", type=int, default=24, help="decode-loop layers")
     ap.add_argument("--merge-first", action="store_true",
-                    help="decode loop, fused mode: rows of merging slots first (default: slot order)")
+                    help="decode loop, fused mode: rows of merging slots first (same as "
+                         "--row-order merge_first)")
+    ap.add_argument("--row-order", default="", choices=("", "slot", "merge_first", "balanced"),
+                    help="row order of a launch whose slots sit at different live lengths "
+                         "(the staggered stack, the decode loop's fused mode): slot order, "
+                         "merging slots first, or by live length, longest first "
+                         "(default: balanced for the kernel bench, slot for the decode loop)")
     ap.add_argument("--uniform", action="store_true",
                     help="decode loop: admit every sequence at once (default: staggered)")
     ap.add_argument("--autotune", type=int, default=0, metavar="MAX_M",
@@ -230,36 +257,100 @@ def copy_ceiling(torch, stream, gib=2, reps=5):
     return 2 * (gib << 30) / (float(np.median(ms)) * 1e-3) / 1e9
 
 
+def host_cpu():
+    """Cores this process may run on, and the CPU model (from /proc/cpuinfo, else lscpu)."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    if model is None:
+        try:
+            import subprocess
+            out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+            m = re.search(r"^Model name:\s*(.+)$", out, flags=re.M)
+            model = m.group(1).strip() if m else None
+        except (OSError, subprocess.SubprocessError):
+            pass
+    return {"affinity_cores": len(os.sched_getaffinity(0)), "cpu_count": os.cpu_count(),
+            "model": model or "unknown"}
+
+
 def cpu_baseline(w, budget_s):
-    """The fp64 oracle eager recurrence, as it stands, on a bounded sample of the same
-    workload shape (the B x H heads of one layer -- at most 64 x 32 x 128^2 -- for as
-    many steps as fit the time budget)."""
+    """The fp64 oracle eager recurrence (Eq. 3), as it stands, on a bounded sample of the
+    workload: one layer of at most 64 x 32 heads of 128^2 (fewer sequences than B where
+    the layer is larger), for up to the workload's decode length or ``budget_s`` seconds.
+    It runs twice: on every core this process may use, the heads split into one chunk per
+    core and stepped by a thread pool (NumPy releases the GIL in its array loops), and on
+    one core.  The rate is in the unit of the GPU value: per-layer token-updates/s, or,
+    for a layer stack, sequence tokens/s through all layers -- the one-layer rate divided
+    by the layer count (an extrapolation: the layers are identical in cost)."""
+    from concurrent.futures import ThreadPoolExecutor
+
     from oracle import eager as OE
     from paper_2608_15533_amd import workloads as W
 
-    B = w.B if w.B * w.H * w.dk * w.dv <= 64 * 32 * 128 * 128 else 64
+    cap = 64 * 32 * 128 * 128
+    B = w.B if w.B * w.H * w.dk * w.dv <= cap else max(1, cap // (w.H * w.dk * w.dv))
     ws = w.with_(B=B)
-    S = W.initial_state(ws).astype(np.float64)
-    xs = [W.step_inputs(ws, t) for t in range(4)]
+    N = B * w.H
+    S0 = W.initial_state(ws).astype(np.float64).reshape(N, w.dk, w.dv)
+    flat = lambda a: None if a is None else a.reshape((N,) + a.shape[2:])
+    xs = [{k: flat(a) for k, a in W.step_inputs(ws, t).items()} for t in range(4)]
     u = W.bonus(ws)
-    u = None if u is None else np.broadcast_to(u, xs[0]["k"].shape)
-    wall0, cpu0 = time.perf_counter(), time.process_time()
-    steps = 0
-    while True:
-        x = xs[steps % len(xs)]
-        S, _ = OE.eager_step(w.op, S, x["q"], x["k"], x["v"], x["beta"], x.get("lam"), u=u)
-        steps += 1
-        el = time.perf_counter() - wall0
-        if el >= budget_s or steps >= 256:
-            break
-    cpu = time.process_time() - cpu0
+    u = None if u is None else np.broadcast_to(u, (B,) + u.shape).reshape(N, w.dk)
+    part = lambda a, lo, hi: None if a is None else a[lo:hi]
+
+    def rollout(threads):
+        S = S0.copy()
+        chunks = [(i * N // threads, (i + 1) * N // threads) for i in range(threads)]
+
+        def one(c, x):
+            lo, hi = c
+            S[lo:hi], _ = OE.eager_step(w.op, S[lo:hi], x["q"][lo:hi], x["k"][lo:hi],
+                                        x["v"][lo:hi], part(x["beta"], lo, hi),
+                                        part(x["lam"], lo, hi), u=part(u, lo, hi))
+
+        steps = 0
+        with ThreadPoolExecutor(threads) as ex:
+            wall0, cpu0 = time.perf_counter(), time.process_time()
+            while True:
+                x = xs[steps % len(xs)]
+                list(ex.map(lambda c: one(c, x), chunks))
+                steps += 1
+                el = time.perf_counter() - wall0
+                if el >= budget_s or steps >= w.steps:
+                    break
+            cpu = time.process_time() - cpu0
+        return steps, el, cpu
+
+    host = host_cpu()
+    cores = host["affinity_cores"]
+    steps_all, el_all, cpu_all = rollout(cores)
+    steps_one, el_one, _ = rollout(1)
+    scale = 1.0 / w.layers                   # sequence tokens through all layers
+    rate = lambda steps, el: round(B * steps / el * scale, 2)
+    unit = ("sequence tokens/s (all layers)" if w.layers > 1 else "tokens/s")
     return {
-        "value": round(B * steps / el, 2),
-        "unit": "tokens/s",
-        "cores": max(1, int(round(cpu / el))),
+        "value": rate(steps_all, el_all),
+        "unit": unit,
+        "cores": cores,
         "kind": "oracle",
-        "sample": f"fp64 eager oracle, {B}x{w.H} heads of {w.dk}x{w.dv}, {steps} decode steps "
-                  f"({el:.1f} s wall, {cpu:.1f} s CPU) on the host of this GPU",
+        "sample": (f"fp64 eager oracle (Eq. 3), one layer of {B} of the {w.B} sequences x "
+                   f"{w.H} heads of {w.dk}x{w.dv}: {steps_all} decode steps on {cores} cores "
+                   f"({el_all:.1f} s wall, {cpu_all:.1f} s CPU; heads split into {cores} "
+                   f"chunks over a thread pool) and {steps_one} steps on one core "
+                   f"({el_one:.1f} s)"
+                   + (f"; the {w.layers}-layer rate is the one-layer rate / {w.layers} "
+                      "(extrapolated)" if w.layers > 1 else "")),
+        "single_core_value": rate(steps_one, el_one),
+        "cpu_model": host["model"],
+        "affinity_cores": cores,
+        "cpu_count": host["cpu_count"],
     }
 
 
@@ -279,7 +370,7 @@ def decode_loop(args):
     M = args.merge_interval or 16
     layers = args.layers
     H, dk, dv = 32, 128, 128
-    K, WU = args.steps, args.warmup
+    K, WU = args.steps or 64, args.warmup
     modes = decode.MODES if args.decode_loop == "all" else tuple(args.decode_loop.split(","))
     desc = D.make_desc("gdn", B, H, dk, dv, M, "bf16")
     torch.cuda.set_device(0)
@@ -287,7 +378,8 @@ def decode_loop(args):
     for mode in modes:
         for graphs in (True, False):
             eng = decode.DecodeEngine(desc, layers, mode=mode, graphs=graphs,
-                                      merge_first=args.merge_first)
+                                      merge_first=args.merge_first,
+                                      row_order=args.row_order or None)
             gen = torch.Generator(device="cuda")
             gen.manual_seed(20261202)
             for layer in range(layers):
@@ -358,7 +450,8 @@ def decode_loop(args):
                                f"dk=dv={dk}, M={M}, bf16 q/k/v, fp32 state, "
                                f"{'uniform' if args.uniform else 'staggered'} admission",
                    "batch": B, "layers": layers, "merge_interval": M,
-                   "fused_row_order": "merging slots first" if args.merge_first else "slot"},
+                   "fused_row_order": (args.row_order or
+                                       ("merge_first" if args.merge_first else "slot"))},
         "modes": res,
         "kernel_source_hash": kernel_source_hash(),
     }), flush=True)
@@ -468,7 +561,9 @@ def main():
                                  + (w.M - 1) * (w.dk + w.dv) * 4)
         R = max(2, -(-(1 << 30) // per_layer)) if w.layers == 1 else R
     R = args.replicas or R
-    K, WU = args.steps, args.warmup
+    K, WU = args.steps or w.steps, args.warmup
+    if K < 1 or WU < 0 or args.repeats < 1:
+        raise SystemExit("--steps, --repeats >= 1 and --warmup >= 0")
     dev = "cuda"
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
@@ -508,11 +603,31 @@ def main():
         assert np.array_equal(live, W.fill_offsets(w))
     torch.cuda.synchronize()
 
+    # Row order of the DeltaLog launches.  With staggered logs the slots of a launch sit
+    # at different live lengths; the balanced order (longest log first, as the decode
+    # scheduler plans it) gives every XCD the same mix.  The order repeats with the merge
+    # interval, so one slot list per phase serves the whole run.
+    row_order = args.row_order or ("balanced" if w.staggered else "slot")
+    PER = POOL
+    lists = None
+    if row_order != "slot":
+        from paper_2608_15533_amd.scheduler import balanced_order
+        PER = int(np.lcm(POOL, w.M))
+        lists = []
+        for k in range(PER):
+            Lk = (live + k) % w.M
+            if row_order == "balanced":
+                order = balanced_order(range(w.B), Lk)
+            else:
+                order = tuple(np.nonzero(Lk == w.M - 1)[0]) + tuple(np.nonzero(Lk < w.M - 1)[0])
+            lists.append(torch.tensor(order, dtype=torch.int32, device=dev))
     dref = ctypes.byref(desc)
     app = D.lib.dl_append_step
     eag = D.lib.dl_eager_step
-    app_args = [[(dref, ctypes.byref(states[r].struct), ctypes.byref(toks[t].struct),
-                  outs[r].data_ptr(), None, w.B, sp) for t in range(POOL)] for r in range(R)]
+    sl_ptr = (lambda k: None) if lists is None else (lambda k: lists[k % PER].data_ptr())
+    app_args = [[(dref, ctypes.byref(states[r].struct), ctypes.byref(toks[k % POOL].struct),
+                  outs[r].data_ptr(), sl_ptr(k), w.B, sp) for k in range(PER)]
+                for r in range(R)]
     if args.tiled:
         # value-tiled path: [ReplayPrep] + tiles + Finalize per layer and step; one
         # scratch buffer serves every layer (the launches are ordered on one stream)
@@ -520,71 +635,84 @@ def main():
         ws = D.tiled_workspace(desc, w.B) if split else None
         wsp, wsn = (None, 0) if ws is None else (ws.data_ptr(), ws.numel())
         app = D.lib.dl_append_step_tiled
-        app_args = [[(dref, ctypes.byref(states[r].struct), ctypes.byref(toks[t].struct),
-                      outs[r].data_ptr(), None, w.B, args.tiled, int(split), wsp, wsn, sp)
-                     for t in range(POOL)] for r in range(R)]
-    eag_args = [[(dref, eager_S[r].data_ptr(), ctypes.byref(toks[t].struct),
-                  outs[r].data_ptr(), None, w.B, sp) for t in range(POOL)] for r in range(R)]
+        app_args = [[(dref, ctypes.byref(states[r].struct), ctypes.byref(toks[k % POOL].struct),
+                      outs[r].data_ptr(), sl_ptr(k), w.B, args.tiled, int(split), wsp, wsn, sp)
+                     for k in range(PER)] for r in range(R)]
+    eag_args = [[(dref, eager_S[r].data_ptr(), ctypes.byref(toks[k % POOL].struct),
+                  outs[r].data_ptr(), None, w.B, sp) for k in range(PER)] for r in range(R)]
 
-    def run(fn, argtab, k0, nsteps, events=None):
+    done = [0]                                           # steps executed so far
+
+    def run(fn, argtab, nsteps, events=None, capture=None):
+        """Launch ``nsteps`` steps (R launches each) from the next step index; with
+        ``capture`` (a stream handle) the launches are recorded, not executed."""
+        k0 = done[0]
         for i, k in enumerate(range(k0, k0 + nsteps)):
             if events is not None:
                 events[i][0].record(stream)
             for r in range(R):
-                rc = fn(*argtab[r][k % POOL])
+                a = argtab[r][k % PER]
+                rc = fn(*(a if capture is None else a[:-1] + (capture,)))
                 if rc != 0:
                     raise D.DeltaLogError(rc, fn.__name__)
             if events is not None:
                 events[i][1].record(stream)
+        if capture is None:
+            done[0] += nsteps
 
-    def with_stream(argtab, handle):
-        return [[a[:-1] + (handle,) for a in row] for row in argtab]
+    def region(body):
+        """One timed region: synchronize, HIP events on the launch stream around
+        ``body``, synchronize; returns elapsed ms."""
+        torch.cuda.synchronize()
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        t0.record(stream)
+        body()
+        t1.record(stream)
+        torch.cuda.synchronize()
+        return t0.elapsed_time(t1)
 
-    def timed(fn, argtab):
-        """W untimed steps, then K timed steps bracketed by synchronize + HIP events on
-        the launch stream; returns elapsed ms (no per-launch events inside).  With
-        --graph the steps are replays of one captured graph of POOL steps."""
-        if not args.graph:
-            run(fn, argtab, 0, WU)
-            torch.cuda.synchronize()
-            t0 = torch.cuda.Event(enable_timing=True)
-            t1 = torch.cuda.Event(enable_timing=True)
-            t0.record(stream)
-            run(fn, argtab, WU, K)
-            t1.record(stream)
-            torch.cuda.synchronize()
-            return t0.elapsed_time(t1)
-        if K % POOL or WU % POOL:
-            raise SystemExit(f"--graph needs --steps and --warmup to be multiples of {POOL}")
-        run(fn, argtab, 0, POOL)                    # load the kernels before capture
+    def timed_direct(fn, argtab, warm):
+        """``warm`` untimed steps, then the timed rollouts of K steps (no per-launch
+        events inside); returns (ms of each rollout, first timed step index)."""
+        run(fn, argtab, warm)
+        first = done[0]
+        return [region(lambda: run(fn, argtab, K)) for _ in range(args.repeats)], first
+
+    graph_possible = K % PER == 0 and WU % PER == 0
+
+    def timed_graph(fn, argtab, warm):
+        """The same rollouts submitted as replays of one captured graph of PER steps x R
+        launches (the kernels loaded by PER direct steps first)."""
+        run(fn, argtab, PER)
         torch.cuda.synchronize()
         g = torch.cuda.CUDAGraph()
         cs = torch.cuda.Stream()
         cs.wait_stream(stream)
         with torch.cuda.stream(cs):
             with torch.cuda.graph(g, stream=cs):
-                run(fn, with_stream(argtab, cs.cuda_stream), 0, POOL)
+                run(fn, argtab, PER, capture=cs.cuda_stream)
         stream.wait_stream(cs)
-        for _ in range(max(WU // POOL - 1, 0)):
-            g.replay()
-        torch.cuda.synchronize()
-        t0 = torch.cuda.Event(enable_timing=True)
-        t1 = torch.cuda.Event(enable_timing=True)
-        t0.record(stream)
-        for _ in range(K // POOL):
-            g.replay()
-        t1.record(stream)
-        torch.cuda.synchronize()
-        return t0.elapsed_time(t1)
 
-    def per_launch(fn, argtab, k0, nsteps):
+        def replays(n):
+            for _ in range(n // PER):
+                g.replay()
+            done[0] += n
+
+        replays(max(warm - PER, 0))
+        first = done[0]
+        ms = [region(lambda: replays(K)) for _ in range(args.repeats)]
+        del g
+        return ms, first
+
+    def per_launch(fn, argtab, nsteps):
         """A separate pass with an event pair around each step's R launches, which share
         one live length (per-phase split): returns the mean launch time of every step, so
         the cost of recording events is spread over R launches instead of inflating each.
         The events are created beforehand so the host keeps ahead of the device."""
         evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
                for _ in range(nsteps)]
-        run(fn, argtab, k0, nsteps, evs)
+        run(fn, argtab, nsteps, evs)
         torch.cuda.synchronize()
         return np.array([a.elapsed_time(b) for a, b in evs]) / R
 
@@ -596,17 +724,31 @@ def main():
                    for L, c in enumerate(counts) if c)
 
     # ------------------------------------------------------------------ DeltaLog
-    dl_ms = timed(app, app_args)
+    primary, secondary = (timed_graph, timed_direct) if args.graph else (timed_direct, timed_graph)
+    if args.graph and not graph_possible:
+        raise SystemExit(f"--graph needs --steps and --warmup to be multiples of {PER}")
+    rollouts, first = primary(app, app_args, WU)
+    dl_ms = float(np.median(rollouts))
     n_launch = K * R
     tokens = w.B * K if w.layers > 1 else w.B * R * K    # stack: tokens through all layers
     dl_tok = tokens / (dl_ms * 1e-3)
-    avg_launch_us = dl_ms * 1e3 / n_launch
-    bytes_per_launch = float(np.mean([launch_bytes(WU + k) for k in range(K)]))
+    # roofline: every timed launch -- all rollouts -- over the time of all rollouts
+    nrep = len(rollouts)
+    avg_launch_us = float(np.sum(rollouts)) * 1e3 / (n_launch * nrep)
+    bytes_per_launch = float(np.mean([launch_bytes(first + k) for k in range(K * nrep)]))
     achieved = bytes_per_launch / (avg_launch_us * 1e-6) / 1e9
+    other = None
+    if graph_possible and not args.single_submission:
+        o_ms, _ = secondary(app, app_args, PER)
+        o_med = float(np.median(o_ms))
+        other = {"submission": "direct launches" if args.graph else "HIP graph replay",
+                 "value": round(tokens / (o_med * 1e-3), 1),
+                 "us_per_step": round(o_med * 1e3 / K, 3),
+                 "rollouts_ms": [round(x, 4) for x in o_ms]}
 
-    k0 = WU + K
     PH = 2 * w.M
-    ph_durs = per_launch(app, app_args, k0, PH)
+    k0 = done[0]
+    ph_durs = per_launch(app, app_args, PH)
     for s in states:
         assert int(s.err.item()) == 0
     phases = {"source": "separate pass, HIP event pair around each step's launches (one per "
@@ -620,11 +762,15 @@ def main():
             by_L[("merge_L%d" if L == w.M - 1 else "append_L%d") % L] = {
                 "us": round(us, 2), "GB/s": round(b / (us * 1e-6) / 1e9, 1)}
         app_sel = np.array([(k0 + k) % w.M < w.M - 1 for k in range(PH)])
-        app_us = float(np.median(ph_durs[app_sel]) * 1e3)
-        app_b = float(np.mean([launch_bytes(k0 + k) for k in range(PH) if app_sel[k]]))
+        phases_out = []
+        if app_sel.any():
+            app_us = float(np.median(ph_durs[app_sel]) * 1e3)
+            app_b = float(np.mean([launch_bytes(k0 + k) for k in range(PH) if app_sel[k]]))
+            phases_out.append(("append", app_us, app_b))
         mrg_us = float(np.median(ph_durs[~app_sel]) * 1e3)
         mrg_b = T.merge_bytes(w.op, w.dk, w.dv, w.M - 1, w.in_dtype, sd).total * heads
-        for name, us, b in (("append", app_us, app_b), ("merge", mrg_us, mrg_b)):
+        phases_out.append(("merge", mrg_us, mrg_b))
+        for name, us, b in phases_out:
             gbs = b / (us * 1e-6) / 1e9
             phases[name] = {"us": round(us, 2), "GB/s": round(gbs, 1),
                             "frac": round(gbs / HBM_PEAK_GBS, 4)}
@@ -636,7 +782,8 @@ def main():
                            "note": "every launch mixes appending and merging slots"}
 
     # ------------------------------------------------------------------ eager baseline
-    eg_ms = timed(eag, eag_args)
+    eg_rollouts, _ = primary(eag, eag_args, WU)
+    eg_ms = float(np.median(eg_rollouts))
     eg_tok = tokens / (eg_ms * 1e-3)
     eg_bytes = T.eager_bytes(w.op, w.dk, w.dv, w.in_dtype, sd).total * heads
     eg_us = eg_ms * 1e3 / n_launch
@@ -678,6 +825,7 @@ def main():
             "op": w.op, "batch": w.B, "heads": w.H, "dk": w.dk,
             "dv": w.dv, "merge_interval": w.M, "in_dtype": w.in_dtype, "state_dtype": sd,
             "layer_states": R, "state_MiB_per_layer": state_mib,
+            "row_order": row_order,
             "working_set_MiB": round(sum(t.numel() * t.element_size() for st in states
                                          for t in st.buffers().values()
                                          if t is not None) / 2**20, 1),
@@ -704,12 +852,22 @@ def main():
             "d2d_copy_GB/s": round(copy_gbs, 1),
             "achieved_vs_d2d_copy": round(achieved / copy_gbs, 4),
             "algorithmic_bytes_per_launch": round(bytes_per_launch, 1),
-            "duration_source": "HIP events around the timed region / launches",
+            "duration_source": "HIP events around each timed rollout: summed over the "
+                               "rollouts / their launches",
+        },
+        "timing": {
+            "submission": "HIP graph replay" if args.graph else "direct launches",
+            "repeats": args.repeats,
+            "rollouts_ms": [round(x, 4) for x in rollouts],
+            "value_from": "median rollout",
+            "us_per_step": round(dl_ms * 1e3 / K, 3),
+            "other_submission": other,
         },
         "phases": phases,
         "eager": {
             "tokens_per_s": round(eg_tok, 1),
             "ms_per_step": round(eg_ms / K, 5),
+            "rollouts_ms": [round(x, 4) for x in eg_rollouts],
             "us_per_launch": round(eg_us, 3),
             "GB/s": round(eg_gbs, 1),
             "frac": round(eg_gbs / HBM_PEAK_GBS, 4),

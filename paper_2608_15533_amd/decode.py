@@ -18,10 +18,12 @@ Scheduling policies (``mode``):
     One ``dl_append_step`` launch per layer over all active slots.  Every workgroup
     takes the append or merge branch of Alg. 1 for its own slot, so a batch whose slots
     sit at different points of their cycles is one launch, and one captured graph per
-    batch size covers both phases.  Rows keep slot order; ``merge_first`` puts the rows
-    of slots that merge in the step first instead, so the longer merging workgroups start
-    before the appending ones (on MI355X this measured no different from slot order,
-    since the kernel deals runs of consecutive heads to the eight XCDs in turn).
+    batch size covers both phases.  ``row_order`` (scheduler) picks the rows' order:
+    slot order; ``"merge_first"``, the rows of slots that merge in the step first, so
+    the longer merging workgroups start before the appending ones; or ``"balanced"``,
+    rows by live length, longest first.  The kernel deals runs of consecutive heads to
+    the eight XCDs in turn, so the last two spread the merges evenly over the XCDs
+    whatever slot ids the merging sequences hold.
 ``"phased"``
     The paper's phase-specialised scheduling (Sec. 4: an append queue and a merge queue,
     append and merge graphs selected by a key that encodes the phase).  Rows are ordered
@@ -100,14 +102,15 @@ class DecodeEngine:
     stepped one decode token at a time under a scheduling ``mode``."""
 
     def __init__(self, desc, layers, mode="fused", graphs=True, device="cuda",
-                 merge_first=False):
+                 merge_first=False, row_order=None):
         if layers < 1:
             raise ValueError("need at least one layer")
         self.desc = desc
         self.layers = layers
         self.graphs = graphs
         self.device = device
-        self.sched = DecodeScheduler(desc.num_slots, desc.merge_interval, mode, merge_first)
+        self.sched = DecodeScheduler(desc.num_slots, desc.merge_interval, mode, merge_first,
+                                     row_order)
         self.states = [D.DeltaLogState(desc, device=device) for _ in range(layers)]
         self.inputs = [LayerInputs(desc, device) for _ in range(layers)]
         self.outputs = [torch.zeros((desc.num_slots, desc.heads, desc.dv),

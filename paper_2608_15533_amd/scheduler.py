@@ -14,6 +14,16 @@ returns to zero at the step that merges (when the log already holds C = M - 1 en
 from dataclasses import dataclass
 
 MODES = ("fused", "phased", "phased_concurrent")
+ROW_ORDERS = ("slot", "merge_first", "balanced")
+
+
+def balanced_order(slots, live):
+    """Rows ordered by live length, longest first (the slots that merge in this step
+    first), ties in slot order.  The kernel deals runs of 32 consecutive (row, head)
+    workgroups to the eight XCDs in turn, so with 32 heads per row, row r runs on XCD
+    r mod 8: dealing the rows in this order gives every XCD the same mix of merges and
+    of log lengths, instead of whatever mix the slot ids happen to have."""
+    return tuple(sorted(slots, key=lambda s: (-live[s], s)))
 
 
 class SlotError(RuntimeError):
@@ -25,8 +35,9 @@ class StepPlan:
     """One decode step: the row order of the launch(es), the append queue and the merge
     queue, and the graph key.  Phased modes order the append queue first, then the
     merge queue.  The fused mode (one launch; the device picks each slot's phase) keeps
-    slot order, or with ``merge_first`` puts the merge queue first so the longer merging
-    workgroups are dispatched before the appending ones."""
+    slot order (``row_order="slot"``), puts the merge queue first (``"merge_first"``) so
+    the longer merging workgroups are dispatched before the appending ones, or orders the
+    rows by live length, longest first (``"balanced"``, see ``balanced_order``)."""
     order: tuple
     append_slots: tuple
     merge_slots: tuple
@@ -51,15 +62,20 @@ class StepPlan:
 class DecodeScheduler:
     """Slot allocator and per-step planner for B slots with merge interval M."""
 
-    def __init__(self, num_slots, merge_interval, mode="fused", merge_first=False):
+    def __init__(self, num_slots, merge_interval, mode="fused", merge_first=False,
+                 row_order=None):
         if mode not in MODES:
             raise ValueError(f"mode must be one of {MODES}")
         if merge_interval < 1:
             raise ValueError("merge interval must be >= 1")
+        row_order = row_order or ("merge_first" if merge_first else "slot")
+        if row_order not in ROW_ORDERS:
+            raise ValueError(f"row order must be one of {ROW_ORDERS}")
         self.B = num_slots
         self.C = merge_interval - 1
         self.mode = mode
-        self.merge_first = merge_first
+        self.row_order = row_order
+        self.merge_first = row_order == "merge_first"
         self.live = [0] * num_slots                 # host mirror of each slot's L
         self.active = []                            # admission order
         self._free = list(range(num_slots))[::-1]   # lowest slot id handed out first
@@ -89,7 +105,10 @@ class DecodeScheduler:
         app = tuple(s for s in act if self.live[s] < self.C)
         mrg = tuple(s for s in act if self.live[s] >= self.C)
         if self.mode == "fused":
-            order = mrg + app if self.merge_first else tuple(act)
+            if self.row_order == "balanced":
+                order = balanced_order(act, self.live)
+            else:
+                order = mrg + app if self.merge_first else tuple(act)
             return StepPlan(order, app, mrg, ("fused", len(act)))
         return StepPlan(app + mrg, app, mrg, (self.mode, len(app), len(mrg)))
 

@@ -64,8 +64,28 @@ def test_profile_keys():
 def test_cpu_baseline_leg_reports_the_contract_fields():
     res = bench.cpu_baseline(W.GDN_SMALL, 0.2)
     assert res["kind"] == "oracle" and res["unit"] == "tokens/s"
-    assert res["value"] > 0 and res["cores"] >= 1
+    assert res["value"] > 0 and res["single_core_value"] > 0
+    assert res["cores"] == res["affinity_cores"] == len(os.sched_getaffinity(0))
+    assert res["cpu_model"]
     assert "fp64 eager oracle" in res["sample"]
+
+
+def test_cpu_baseline_of_the_layer_stack_is_a_bounded_one_layer_sample():
+    """The 24-layer stack is timed on one layer of 64 of its 256 sequences and reported
+    in sequence tokens/s through all layers, the extrapolation stated."""
+    res = bench.cpu_baseline(W.GDN_STACK, 0.01)
+    assert res["unit"] == "sequence tokens/s (all layers)"
+    assert "64 of the 256 sequences" in res["sample"]
+    assert "rate / 24 (extrapolated)" in res["sample"]
+
+
+def test_small_latency_workloads_are_benchmarked():
+    wl = bench.workloads()
+    for name in ("gdn_b1_h2_d64_m8", "gdn_b1_h2_d64_m8_bf16"):
+        w, R = wl[name]
+        assert (w.B, w.H, w.dk, w.dv, w.M, w.steps, R) == (1, 2, 64, 64, 8, 64, 1)
+    assert wl["gdn_b1_h2_d64_m8"][0].in_dtype == "f32"
+    assert wl["gdn_b1_h2_d64_m8_bf16"][0].in_dtype == "bf16"
 
 
 def test_kernel_source_hash_is_stable():

@@ -10,7 +10,7 @@ import random
 
 import pytest
 
-from paper_2608_15533_amd.scheduler import MODES, DecodeScheduler, SlotError
+from paper_2608_15533_amd.scheduler import balanced_order, MODES, DecodeScheduler, SlotError
 
 
 def test_allocator_hands_out_lowest_free_slot_and_rejects_misuse():
@@ -55,6 +55,37 @@ def test_fused_plan_puts_merging_slots_first():
     s.commit(p)                        # a, b restart at 0; c reaches L = C
     p = s.plan()
     assert p.merge_slots == (c,) and p.order == (c, a, b)
+
+
+def test_balanced_plan_orders_rows_by_live_length_longest_first():
+    """Balanced row order: merging slots first, then by decreasing live length, ties in
+    slot order; the same slots and queues as slot order, only the rows move."""
+    s = DecodeScheduler(6, 4, "fused", row_order="balanced")
+    slots = [s.admit() for _ in range(6)]
+    s.live[:] = [1, 3, 0, 2, 3, 1]
+    p = s.plan()
+    assert p.order == (1, 4, 3, 0, 5, 2)
+    assert p.merge_slots == (1, 4) and p.append_slots == (0, 2, 3, 5)
+    assert p.key == ("fused", 6)
+    assert balanced_order(slots, s.live) == p.order
+    with pytest.raises(ValueError):
+        DecodeScheduler(2, 4, "fused", row_order="bogus")
+
+
+def test_balanced_order_spreads_merges_over_the_xcds():
+    """With 32 heads per row the kernel runs row r on XCD r mod 8: at any stagger the
+    balanced order gives each XCD an equal share of the merging slots (within one)."""
+    import numpy as np
+    rng = np.random.default_rng(5)
+    M = 16
+    off = rng.integers(0, M, size=256)
+    for k in range(M):
+        live = (off + k) % M
+        order = balanced_order(range(256), live)
+        per_xcd = np.zeros(8, dtype=int)
+        for r, slot in enumerate(order):
+            per_xcd[r % 8] += live[slot] == M - 1
+        assert per_xcd.max() - per_xcd.min() <= 1, (k, per_xcd)
 
 
 def test_uniform_batch_alternates_append_and_merge_graph_keys():
