@@ -99,6 +99,8 @@ def parse():
     ap.add_argument("--graph", action="store_true",
                     help="submit the timed steps as replays of one HIP graph holding 16 steps "
                          "x R launches (the same launches, captured once)")
+    ap.add_argument("--phase-cycles", type=int, default=2,
+                    help="merge cycles of the per-phase pass (event pair around each step)")
     ap.add_argument("--single-submission", action="store_true",
                     help="time only the chosen submission (direct launches, or --graph), "
                          "not the other one as well (counter runs)")
@@ -746,7 +748,7 @@ def main():
                  "us_per_step": round(o_med * 1e3 / K, 3),
                  "rollouts_ms": [round(x, 4) for x in o_ms]}
 
-    PH = 2 * w.M
+    PH = args.phase_cycles * w.M
     k0 = done[0]
     ph_durs = per_launch(app, app_args, PH)
     for s in states:

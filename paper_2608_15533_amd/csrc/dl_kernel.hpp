@@ -178,6 +178,34 @@ __device__ __forceinline__ float dl_exp(float x) { return __expf(x); }
 #ifndef DL_KT_ROW_ORDER
 #define DL_KT_ROW_ORDER 1
 #endif
+// Order of the per-row token vectors the coefficient pass reads (k, q and the per-key
+// log-decays) in LDS: row r = c * RPL + x (run c, element x) at position x * LPE + c (1),
+// or at r (0).  A coefficient pass reads element x of every run at once, RPL rows
+// apart: in row order the 16 lanes of an entry meet in a few banks, in this order they
+// read consecutive words.
+#ifndef DL_COEF_LDS_ORDER
+#define DL_COEF_LDS_ORDER 1
+#endif
+// Long logs.  The STEP and MERGE kernels come in two builds: one for a capacity of at
+// most one coefficient pass (C <= 16), and one for longer logs, chosen by the host from
+// the descriptor's merge interval.  Only the long build carries the machinery below, so
+// the registers and LDS of the short build stay as they are.
+//   DL_STAGE_CHUNKS        merge chunks of decayed log keys staged in LDS by the
+//                          coefficient passes themselves (same loads and exps); later
+//                          chunks are staged from global memory.
+//   DL_PREFETCH_NEXT_PASS  load the next coefficient pass's log keys (1: and snapshots;
+//                          2: keys only) while the current pass computes.
+//   DL_U_EARLY             load the log values of the next merge chunk before
+//                          contracting the current one.
+#ifndef DL_STAGE_CHUNKS
+#define DL_STAGE_CHUNKS 2
+#endif
+#ifndef DL_PREFETCH_NEXT_PASS
+#define DL_PREFETCH_NEXT_PASS 1
+#endif
+#ifndef DL_U_EARLY
+#define DL_U_EARLY 1
+#endif
 // Issue order of the log entries relative to the state tile (see the kernel).
 #ifndef DL_LOG_FIRST
 #define DL_LOG_FIRST 0
@@ -390,7 +418,7 @@ struct OpTraits {
   static constexpr bool BONUS = OP == OP_RWKV6;   // pre-update readout plus r^T diag(u) k v^T
 };
 
-template <int OP, int DK, int DV, int MODE>
+template <int OP, int DK, int DV, int MODE, bool LONG = false>
 struct Cfg {
   static constexpr int RPT = rows_per_thread(DK, DV);   // state rows held per thread
   static constexpr int NCG = DV / 4;             // float4 column groups
@@ -403,6 +431,12 @@ struct Cfg {
   static constexpr int RPL = DK / LPE;           // key rows per lane (coefficient pass)
   static constexpr int CH = 16;                  // log entries staged per merge chunk
   static constexpr int KTS = CH + 4;             // LDS row stride of the staged K~ chunk
+  // K~ chunks staged by the coefficient passes.  With per-key decay the long build keeps
+  // one: the second chunk's staging slows every append (measured), and the merge stages
+  // the later chunks itself, one chunk ahead.
+  static constexpr int NSTAGE = (LONG && !OpTraits<OP>::PER_KEY) ? DL_STAGE_CHUNKS : 1;
+  static constexpr bool U_EARLY = LONG && DL_U_EARLY;      // (fp32 state only: see kernel)
+  static constexpr int UPT = CH * NCG / NT;     // log-value quads per thread and merge chunk
   static constexpr bool DELTA = OpTraits<OP>::DELTA;
   static constexpr bool DECAY = OpTraits<OP>::DECAY;
   static constexpr bool BONUS = OpTraits<OP>::BONUS;
@@ -419,7 +453,9 @@ struct Cfg {
   static_assert(NT >= DK, "one thread per key row in the prologue");
   static_assert(RPL == 4 || RPL == 8 || RPL == 16, "coefficient pass run length");
   static_assert(NRG % RPL == 0 || RPL % NRG == 0, "row groups and coefficient runs nest");
-  static_assert(CH == EPP, "the first merge chunk is staged by the first coefficient pass");
+  static_assert(CH == EPP, "merge chunk c is staged by coefficient pass c");
+  static_assert(CH * NCG % NT == 0 && UPT >= 1, "whole log-value quads per thread");
+  static_assert(NSTAGE >= 1 && NSTAGE <= 4, "staged merge chunks");
   // LDS row of key row r in the staged K~ chunk (a permutation of [0, DK)), and the
   // same for the two ways the kernel names a row: element x of coefficient run c, and
   // row j of row group rg (rg + NRG j), written so that the part that depends on x or j
@@ -430,10 +466,26 @@ struct Cfg {
   static __device__ __forceinline__ int kt_row_run(int c, int x) {
     return DL_KT_ROW_ORDER ? x * LPE + c : c * RPL + x;
   }
+  // LDS position of token row r in the vectors the coefficient pass reads (the same
+  // permutation as the K~ rows).
+  static __device__ __forceinline__ int cp_pos(int r) {
+    return DL_COEF_LDS_ORDER ? (r % RPL) * LPE + r / RPL : r;
+  }
+  static __device__ __forceinline__ int cp_pos_run(int c, int x) {
+    return DL_COEF_LDS_ORDER ? x * LPE + c : c * RPL + x;
+  }
+  static __device__ __forceinline__ int cp_pos_group(int rg, int j) {
+    if constexpr (!DL_COEF_LDS_ORDER) return rg + NRG * j;
+    else return kt_row_group_order(rg, j);
+  }
   static __device__ __forceinline__ int kt_row_group(int rg, int j) {
-    if constexpr (!DL_KT_ROW_ORDER) {
-      return rg + NRG * j;
-    } else if constexpr (NRG % RPL == 0) {
+    if constexpr (!DL_KT_ROW_ORDER) return rg + NRG * j;
+    else return kt_row_group_order(rg, j);
+  }
+  // (rg + NRG j) % RPL * LPE + (rg + NRG j) / RPL, with the part that depends on j a
+  // compile-time constant.
+  static __device__ __forceinline__ int kt_row_group_order(int rg, int j) {
+    if constexpr (NRG % RPL == 0) {
       return (rg % RPL) * LPE + rg / RPL + (NRG / RPL) * j;
     } else {
       constexpr int q = RPL / NRG;                  // RPL is a multiple of NRG
@@ -464,10 +516,10 @@ constexpr int waves_target(int dk, int dv) {
 // Every global load a workgroup needs is issued before its first barrier: the token
 // rows, the state tile, the first pass of log keys/snapshots and the first log values
 // of the replay; only the live length (and the slot id, for slot lists) precede them.
-template <int OP, int DK, int DV, int MODE, typename TIN, typename TS>
+template <int OP, int DK, int DV, int MODE, typename TIN, typename TS, bool LONG>
 __global__ __launch_bounds__(threads_per_head(DK, DV)) DL_OCCUPANCY
 void deltalog_kernel(KParams p) {
-  using CF = Cfg<OP, DK, DV, MODE>;
+  using CF = Cfg<OP, DK, DV, MODE, LONG>;
   using TU = typename UType<OP, TIN>::type;
   constexpr int NT = CF::NT, NCG = CF::NCG, NRG = CF::NRG, RPT = CF::RPT, DL = CF::DL;
   constexpr int RPL = CF::RPL;
@@ -483,7 +535,10 @@ void deltalog_kernel(KParams p) {
   __shared__ float s_gq[DL_MAX_MERGE_INTERVAL];
   __shared__ float s_red[CF::NW][2][DV];
   __shared__ float s_dotw[CF::NW];
-  __shared__ float s_kt[CF::MERGES_LOG ? DK * CF::KTS : 1];          // K~ chunk [DK][KTS]
+  // K~ chunks [NSTAGE][DK][KTS]: staged by the coefficient passes where the kernel
+  // replays the log, else (flush) one chunk at a time from global memory
+  constexpr int kKtChunks = CF::REPLAYS ? CF::NSTAGE : 1;
+  __shared__ float s_kt[CF::MERGES_LOG ? kKtChunks * DK * CF::KTS : 1];
   __shared__ float4 s_u[CF::MERGES_LOG ? CF::CH * NCG : 1];          // U chunk  [CH][NCG]
 
   const int tid = threadIdx.x;
@@ -661,14 +716,15 @@ void deltalog_kernel(KParams p) {
       lm = ell;
     }
     const float er = dl_exp(lr);
-    s_kf[r0] = kf;
-    s_qf[r0] = qf;
+    const int pr = CF::cp_pos(r0);                // coefficient-pass order
+    s_kf[pr] = kf;
+    s_qf[pr] = qf;
     s_xk[r0] = er * kf;
     s_xq[r0] = er * qf;
     s_em[r0] = dl_exp(lm);
-    if (r0 < DL) {
-      s_lr[r0] = lr;
-      s_lm[r0] = lm;
+    if (r0 < DL) {                                // DL == 1: r0 == 0 == pr
+      s_lr[pr] = lr;
+      s_lm[pr] = lm;
     }
   }
   if constexpr (CF::HAS_TOKEN) {
@@ -681,33 +737,73 @@ void deltalog_kernel(KParams p) {
   __syncthreads();
 
   // ---- 5. replay coefficients g_i(k), g_i(q) of the live entries --------------------
-  // A merging workgroup also writes the first chunk of decayed keys
-  // K~_i[r] = e^(l'_r - Lam_i,r) K_i[r] to LDS here, from the same loads (the merge
-  // decay l' equals the readout decay, except for RWKV6, which reads at ell).
+  // A merging workgroup also writes the decayed keys K~_i[r] = e^(l'_r - Lam_i,r) K_i[r]
+  // of the first NSTAGE chunks to LDS here, from the same loads and exps (the merge
+  // decay l' equals the readout decay, except for RWKV6, which reads at ell).  With
+  // DL_PREFETCH_NEXT_PASS the next pass's keys and snapshots are loaded before the
+  // current pass computes.
   if constexpr (CF::REPLAYS) {
+    constexpr bool kFirstPrefetched = DL_PREFETCH_KEYS && (DL == 1 || kPrefetchPerKey);
+    // The next pass is prefetched where the registers allow it at full occupancy: one
+    // log-decay per head (a scalar snapshot), or small heads; a 128-row per-key head
+    // would need 12 more registers across the pass (one wave per SIMD less).
+    constexpr int kNext = (LONG && (DL == 1 || RPT <= 8)) ? DL_PREFETCH_NEXT_PASS : 0;
+    RawRun<TIN, RPL> kn_raw{};
+    RawRun<float, (DL == 1) ? 8 : RPL> ln_raw{};
+    float ln0 = 0.f;
+    bool next_ready = false;                      // uniform
     for (int i0 = 0; i0 < L; i0 += CF::EPP) {     // uniform trip count
       const int i = i0 + e_;
-      const bool stage = CF::MERGES_LOG && merging && i0 == 0;
+      const int chunk = i0 / CF::CH;
+      const bool stage = CF::MERGES_LOG && merging && chunk < kKtChunks;
+      float* const kt = s_kt + (stage ? chunk : 0) * DK * CF::KTS;
       float ak = 0.f, aq = 0.f;
-      if (i < L) {
-        if (i0 > 0 || !DL_PREFETCH_KEYS || (DL != 1 && !kPrefetchPerKey)) {
-          ld_run<RPL>(Kb + size_t(i) * DK + c_ * RPL, kr);
-          if constexpr (DL == 1) {
-            if constexpr (CF::DECAY) lr_[0] = Lb[size_t(i) * LS];
-          } else {
-            ld_run<RPL>(Lb + size_t(i) * DK + c_ * RPL, lr_);
-          }
+      const bool from_next = next_ready;
+      const bool from_first = kFirstPrefetched && i0 == 0;
+      constexpr bool kNextSnap = kNext == 1;      // snapshots prefetched too
+      if (i < L && !from_next && !from_first) {
+        ld_run<RPL>(Kb + size_t(i) * DK + c_ * RPL, kr);
+      }
+      if (i < L && !from_first && !(from_next && kNextSnap)) {
+        if constexpr (DL == 1) {
+          if constexpr (CF::DECAY) lr_[0] = Lb[size_t(i) * LS];
         } else {
-          kr_raw.get(kr);
-          if constexpr (DL == 1) lr_[0] = lr0;
-          else lr_raw.get(lr_);
+          ld_run<RPL>(Lb + size_t(i) * DK + c_ * RPL, lr_);
         }
+      }
+      if (from_next) {
+        kn_raw.get(kr);
+        if constexpr (kNextSnap) {
+          if constexpr (DL == 1) lr_[0] = ln0;
+          else ln_raw.get(lr_);
+        }
+      } else if (from_first) {
+        kr_raw.get(kr);
+        if constexpr (DL == 1) lr_[0] = lr0;
+        else lr_raw.get(lr_);
+      }
+      next_ready = false;
+      if constexpr (kNext > 0) {
+        if (i0 + CF::EPP < L) {                   // uniform
+          const int en = min(i + CF::EPP, L - 1);
+          kn_raw.load(Kb + size_t(en) * DK + c_ * RPL);
+          if constexpr (kNextSnap) {
+            if constexpr (DL == 1) {
+              if constexpr (CF::DECAY) ln0 = Lb[size_t(en) * LS];
+            } else {
+              ln_raw.load(Lb + size_t(en) * DK + c_ * RPL);
+            }
+          }
+          next_ready = true;
+        }
+      }
+      if (i < L) {
         if constexpr (DL == 1) {
 #pragma unroll
           for (int x = 0; x < RPL; ++x) {
-            const int r = c_ * RPL + x;
-            if constexpr (CF::NEEDS_C) ak = fmaf(kr[x], s_kf[r], ak);
-            aq = fmaf(kr[x], s_qf[r], aq);
+            const int pr = CF::cp_pos_run(c_, x);
+            if constexpr (CF::NEEDS_C) ak = fmaf(kr[x], s_kf[pr], ak);
+            aq = fmaf(kr[x], s_qf[pr], aq);
           }
           const float w = CF::DECAY ? dl_exp(s_lr[0] - lr_[0]) : 1.f;
           if constexpr (CF::NEEDS_C) ak *= w;
@@ -715,25 +811,25 @@ void deltalog_kernel(KParams p) {
           if (stage) {
 #pragma unroll
             for (int x = 0; x < RPL; ++x) {
-              s_kt[CF::kt_row_run(c_, x) * CF::KTS + e_] = w * kr[x];
+              kt[CF::kt_row_run(c_, x) * CF::KTS + e_] = w * kr[x];
             }
           }
         } else {
 #pragma unroll 2
           for (int x = 0; x < RPL; ++x) {
-            const int r = c_ * RPL + x;
-            const float wk = dl_exp(s_lr[r] - lr_[x]) * kr[x];
-            if constexpr (CF::NEEDS_C) ak = fmaf(wk, s_kf[r], ak);
-            aq = fmaf(wk, s_qf[r], aq);
+            const int pr = CF::cp_pos_run(c_, x);
+            const float wk = dl_exp(s_lr[pr] - lr_[x]) * kr[x];
+            if constexpr (CF::NEEDS_C) ak = fmaf(wk, s_kf[pr], ak);
+            aq = fmaf(wk, s_qf[pr], aq);
             if (stage)
-              s_kt[CF::kt_row_run(c_, x) * CF::KTS + e_] =
-                  CF::BONUS ? dl_exp(s_lm[r] - lr_[x]) * kr[x] : wk;
+              kt[CF::kt_row_run(c_, x) * CF::KTS + e_] =
+                  CF::BONUS ? dl_exp(s_lm[pr] - lr_[x]) * kr[x] : wk;
           }
         }
       } else if (stage) {
 #pragma unroll
         for (int x = 0; x < RPL; ++x) {
-          s_kt[CF::kt_row_run(c_, x) * CF::KTS + e_] = 0.f;
+          kt[CF::kt_row_run(c_, x) * CF::KTS + e_] = 0.f;
         }
       }
       if constexpr (CF::NEEDS_C) ak = group_sum<CF::LPE>(ak);   // the delta-rule correction only
@@ -838,7 +934,7 @@ void deltalog_kernel(KParams p) {
         reinterpret_cast<uint4*>(Kd)[x] = reinterpret_cast<const uint4*>(kin)[x];
       if constexpr (CF::DECAY) {
         for (int x = tid; x < DL; x += NT) {
-          Lw[size_t(L) * LS + x] = s_lm[x];
+          Lw[size_t(L) * LS + x] = s_lm[CF::cp_pos(x)];
         }
       }
       if (tid == 0) p.len[sh] = L + 1;
@@ -853,33 +949,83 @@ void deltalog_kernel(KParams p) {
     for (int j = 0; j < RPT; ++j) {
       const int r = rg + NRG * j;
       m[j] = s_em[r] * t[j].get();
-      if constexpr (CF::HAS_TOKEN) m[j] = fma4(s_kf[r], bv, m[j]);
+      if constexpr (CF::HAS_TOKEN) m[j] = fma4(s_kf[CF::cp_pos_group(rg, j)], bv, m[j]);
     }
     if constexpr (CF::MERGES_LOG) {
-      for (int i0 = 0; i0 < L; i0 += CF::CH) {     // uniform trip count
-        const int n = min(CF::CH, L - i0);
-        __syncthreads();                            // previous chunk consumed / chunk 0 visible
-        if (CF::REPLAYS && i0 == 0) goto contract;  // chunk 0 was staged during the replay
-#pragma unroll 2
-        for (int x = tid; x < DK * CF::CH; x += NT) {
-          const int r = x % DK, ii = x / DK;
-          float val = 0.f;
-          if (ii < n) {
-            const int i = i0 + ii;
-            val = ld1(Kb + size_t(i) * DK + r);
-            if constexpr (CF::DECAY) {
-              const float lam_i = Lb[size_t(i) * LS + ((DL == 1) ? 0 : r)];
-              val *= dl_exp(s_lm[(DL == 1) ? 0 : r] - lam_i);
-            }
+      // Log values of chunk c >= 1 (chunk 0 was staged by the replay): UPT quads per
+      // thread, loaded before the previous chunk's contraction where DL_U_EARLY.
+      constexpr int UPT = CF::UPT;
+      float4 ur[UPT];
+      auto load_u = [&](int c0) {
+#pragma unroll
+        for (int k = 0; k < UPT; ++k) {
+          const int x = tid + k * NT, ii = x / NCG, c4 = x % NCG;
+          ur[k] = (c0 + ii < L) ? ld4(Ub + size_t(c0 + ii) * DV + 4 * c4) : f4(0.f);
+        }
+      };
+      const int first_global = CF::REPLAYS ? CF::CH : 0;   // first chunk whose U is loaded here
+      // A bf16 state leaves no registers for holding the next chunk's values.
+      constexpr bool kUEarly = CF::U_EARLY && sizeof(TS) == 4;
+      if (kUEarly && first_global < L) load_u(first_global);
+      // Decayed keys of the chunks the coefficient passes did not stage: the same run
+      // layout as the passes (entry e_ of the chunk, rows c_ RPL .. c_ RPL + RPL - 1, one
+      // 16-byte key load and the snapshots of the run), loaded one chunk ahead where
+      // kUEarly, and written to LDS chunk slot 0 (free once chunk 0 is contracted).
+      RawRun<TIN, RPL> kg_raw{};
+      RawRun<float, (DL == 1) ? 8 : RPL> lg_raw{};
+      float lg0 = 0.f;
+      auto load_kt = [&](int c0) {
+        const int ig = min(c0 + e_, L - 1);       // lanes past L re-read entry L-1 (unused)
+        kg_raw.load(Kb + size_t(ig) * DK + c_ * RPL);
+        if constexpr (CF::DECAY) {
+          if constexpr (DL == 1) lg0 = Lb[size_t(ig) * LS];
+          else lg_raw.load(Lb + size_t(ig) * DK + c_ * RPL);
+        }
+      };
+      auto store_kt = [&](int c0) {
+        float kv[RPL];
+        kg_raw.get(kv);
+        const bool live = c0 + e_ < L;
+        if constexpr (DL == 1) {
+          const float w = live ? (CF::DECAY ? dl_exp(s_lm[0] - lg0) : 1.f) : 0.f;
+#pragma unroll
+          for (int x = 0; x < RPL; ++x) s_kt[CF::kt_row_run(c_, x) * CF::KTS + e_] = w * kv[x];
+        } else {
+          float lv[RPL];
+          lg_raw.get(lv);
+#pragma unroll
+          for (int x = 0; x < RPL; ++x) {
+            const float w = live ? dl_exp(s_lm[CF::cp_pos_run(c_, x)] - lv[x]) : 0.f;
+            s_kt[CF::kt_row_run(c_, x) * CF::KTS + e_] = w * kv[x];
           }
-          s_kt[CF::kt_row(r) * CF::KTS + ii] = val;  // K~_i[r] = e^(l'_r - Lam_i,r) K_i[r]
         }
-        for (int x = tid; x < CF::CH * NCG; x += NT) {
-          const int ii = x / NCG, c4 = x % NCG;
-          s_u[x] = (ii < n) ? ld4(Ub + size_t(i0 + ii) * DV + 4 * c4) : f4(0.f);
+      };
+      const int first_kt = CF::REPLAYS ? CF::NSTAGE * CF::CH : 0;   // first chunk staged here
+      // Keys and snapshots one chunk ahead only where they fit beside the contraction's
+      // registers at full occupancy (one log-decay per head, or small heads); a 128-row
+      // per-key head loads them after the barrier (recently read: L2 hits).
+      constexpr bool kKtEarly = kUEarly && CF::NSTAGE == 1 && (DL == 1 || RPT <= 8);
+      if (kKtEarly && first_kt < L) load_kt(first_kt);
+      for (int i0 = 0; i0 < L; i0 += CF::CH) {     // uniform trip count
+        const int chunk = i0 / CF::CH;
+        const int n = min(CF::CH, L - i0);
+        const bool kt_staged = CF::REPLAYS && chunk < CF::NSTAGE;
+        const float* const kt = s_kt + (kt_staged ? chunk : 0) * DK * CF::KTS;
+        __syncthreads();                            // previous chunk consumed / chunk 0 visible
+        if (!(CF::REPLAYS && chunk == 0)) {
+          if (!kt_staged) {                         // K~_i[r] = e^(l'_r - Lam_i,r) K_i[r]
+            if (!kKtEarly) load_kt(i0);
+            store_kt(i0);
+          }
+          if (!kUEarly) load_u(i0);
+#pragma unroll
+          for (int k = 0; k < UPT; ++k) s_u[tid + k * NT] = ur[k];
+          if (kUEarly && i0 + CF::CH < L) {         // the next chunk, in flight meanwhile
+            load_u(i0 + CF::CH);
+            if (kKtEarly && i0 + CF::CH >= first_kt) load_kt(i0 + CF::CH);
+          }
+          __syncthreads();
         }
-        __syncthreads();
-      contract:
         for (int ii = 0; ii < n; ii += 4) {          // zero-padded to a multiple of 4
           const float4 u0 = s_u[(ii + 0) * NCG + cg];
           const float4 u1 = s_u[(ii + 1) * NCG + cg];
@@ -887,12 +1033,12 @@ void deltalog_kernel(KParams p) {
           const float4 u3 = s_u[(ii + 3) * NCG + cg];
 #pragma unroll
           for (int j = 0; j < RPT; ++j) {
-            const float4 kt =
-                *reinterpret_cast<const float4*>(&s_kt[CF::kt_row_group(rg, j) * CF::KTS + ii]);
-            m[j] = fma4(kt.x, u0, m[j]);
-            m[j] = fma4(kt.y, u1, m[j]);
-            m[j] = fma4(kt.z, u2, m[j]);
-            m[j] = fma4(kt.w, u3, m[j]);
+            const float4 k4 =
+                *reinterpret_cast<const float4*>(&kt[CF::kt_row_group(rg, j) * CF::KTS + ii]);
+            m[j] = fma4(k4.x, u0, m[j]);
+            m[j] = fma4(k4.y, u1, m[j]);
+            m[j] = fma4(k4.z, u2, m[j]);
+            m[j] = fma4(k4.w, u3, m[j]);
           }
         }
       }

@@ -5,15 +5,26 @@
 
 namespace dl {
 
-template <int OP, int DK, int DV, int MODE, typename TIN, typename TS>
-hipError_t launch_one(const KParams& p, hipStream_t s) {
-  using CF = Cfg<OP, DK, DV, MODE>;
+template <int OP, int DK, int DV, int MODE, typename TIN, typename TS, bool LONG>
+hipError_t launch_build(const KParams& p, hipStream_t s) {
+  using CF = Cfg<OP, DK, DV, MODE, LONG>;
   const dim3 grid(unsigned(p.n) * unsigned(p.H));
   const dim3 block(CF::NT);
   KParams arg = p;
   void* args[] = {&arg};
-  return hipLaunchKernel(reinterpret_cast<const void*>(&deltalog_kernel<OP, DK, DV, MODE, TIN, TS>),
-                         grid, block, args, 0, s);
+  return hipLaunchKernel(
+      reinterpret_cast<const void*>(&deltalog_kernel<OP, DK, DV, MODE, TIN, TS, LONG>), grid,
+      block, args, 0, s);
+}
+
+// The STEP and MERGE kernels have a second build for logs longer than one coefficient
+// pass (capacity C > 16), picked from the descriptor's merge interval.
+template <int OP, int DK, int DV, int MODE, typename TIN, typename TS>
+hipError_t launch_one(const KParams& p, hipStream_t s) {
+  constexpr bool kHasLong = MODE == M_STEP || MODE == M_MERGE;
+  if (kHasLong && p.C > Cfg<OP, DK, DV, MODE>::CH)
+    return launch_build<OP, DK, DV, MODE, TIN, TS, kHasLong>(p, s);
+  return launch_build<OP, DK, DV, MODE, TIN, TS, false>(p, s);
 }
 
 template <int OP, int DK, int DV, typename TIN, typename TS>
