@@ -436,6 +436,11 @@ struct Cfg {
   // the later chunks itself, one chunk ahead.
   static constexpr int NSTAGE = (LONG && !OpTraits<OP>::PER_KEY) ? DL_STAGE_CHUNKS : 1;
   static constexpr bool U_EARLY = LONG && DL_U_EARLY;      // (fp32 state only: see kernel)
+  // The short build of STEP and MERGE only runs with a capacity of at most one pass
+  // (C <= CH); the other modes run with any capacity.
+  static constexpr bool CAP_ONE_PASS = (MODE == M_STEP || MODE == M_MERGE) && !LONG;
+  // A row group sees a second live entry (row group rg replays rg, rg + NRG, ...).
+  static constexpr bool TWO_PER_GROUP = !(CAP_ONE_PASS && NRG >= CH);
   static constexpr int UPT = CH * NCG / NT;     // log-value quads per thread and merge chunk
   static constexpr bool DELTA = OpTraits<OP>::DELTA;
   static constexpr bool DECAY = OpTraits<OP>::DECAY;
@@ -679,7 +684,7 @@ void deltalog_kernel(KParams p) {
   Raw4<TU> up0_raw{}, up1_raw{};                     // first two replay values of this row group
   if constexpr (CF::REPLAYS && DL_PREFETCH_U) {
     up0_raw.load(Up + size_t(min(rg, Lm1)) * DV + 4 * cg);
-    up1_raw.load(Up + size_t(min(rg + NRG, Lm1)) * DV + 4 * cg);
+    if constexpr (CF::TWO_PER_GROUP) up1_raw.load(Up + size_t(min(rg + NRG, Lm1)) * DV + 4 * cg);
   }
   if constexpr (DL_LOG_FIRST) {
     sched_fence();
@@ -862,7 +867,7 @@ void deltalog_kernel(KParams p) {
         ov = fma4(s_gq[rg], up0, ov);
         if (stage_u && rg < CF::CH) s_u[rg * NCG + cg] = up0;
       }
-      if (DL_PREFETCH_U && rg + NRG < L) {
+      if (CF::TWO_PER_GROUP && DL_PREFETCH_U && rg + NRG < L) {
         if constexpr (CF::NEEDS_C) cv = fma4(s_gk[rg + NRG], up1, cv);
         ov = fma4(s_gq[rg + NRG], up1, ov);
         if (stage_u && rg + NRG < CF::CH) s_u[(rg + NRG) * NCG + cg] = up1;
