@@ -115,7 +115,8 @@ def parse():
     ap.add_argument("--merge-first", action="store_true",
                     help="decode loop, fused mode: rows of merging slots first (same as "
                          "--row-order merge_first)")
-    ap.add_argument("--row-order", default="", choices=("", "slot", "merge_first", "balanced"),
+    ap.add_argument("--row-order", default="", choices=("", "slot", "merge_first", "balanced",
+                                                         "interleaved"),
                     help="row order of a launch whose slots sit at different live lengths "
                          "(the staggered stack, the decode loop's fused mode): slot order, "
                          "merging slots first, or by live length, longest first "
@@ -613,13 +614,15 @@ def main():
     PER = POOL
     lists = None
     if row_order != "slot":
-        from paper_2608_15533_amd.scheduler import balanced_order
+        from paper_2608_15533_amd.scheduler import balanced_order, interleaved_order
         PER = int(np.lcm(POOL, w.M))
         lists = []
         for k in range(PER):
             Lk = (live + k) % w.M
             if row_order == "balanced":
                 order = balanced_order(range(w.B), Lk)
+            elif row_order == "interleaved":
+                order = interleaved_order(range(w.B), Lk)
             else:
                 order = tuple(np.nonzero(Lk == w.M - 1)[0]) + tuple(np.nonzero(Lk < w.M - 1)[0])
             lists.append(torch.tensor(order, dtype=torch.int32, device=dev))

@@ -14,7 +14,7 @@ returns to zero at the step that merges (when the log already holds C = M - 1 en
 from dataclasses import dataclass
 
 MODES = ("fused", "phased", "phased_concurrent")
-ROW_ORDERS = ("slot", "merge_first", "balanced")
+ROW_ORDERS = ("slot", "merge_first", "balanced", "interleaved")
 
 
 def balanced_order(slots, live):
@@ -24,6 +24,27 @@ def balanced_order(slots, live):
     r mod 8: dealing the rows in this order gives every XCD the same mix of merges and
     of log lengths, instead of whatever mix the slot ids happen to have."""
     return tuple(sorted(slots, key=lambda s: (-live[s], s)))
+
+
+def interleaved_order(slots, live, xcds=8):
+    """The balanced order's share for each XCD (every xcds-th row of it), but each XCD's
+    rows taken in bit-reversed order over its dispatch sequence, so the merging and the
+    long-log rows are spread over the launch instead of all starting first."""
+    bal = balanced_order(slots, live)
+    n = len(bal)
+    per = -(-n // xcds)                       # rows per XCD (the last round may be short)
+    bits = max(1, (per - 1).bit_length())
+    rev = sorted(range(per), key=lambda t: int(format(t, f"0{bits}b")[::-1], 2))
+    out = []
+    for t in range(per):                      # dispatch round t
+        for x in range(xcds):                 # row t * xcds + x runs on XCD x
+            i = x + xcds * rev[t]
+            if i < n:
+                out.append(bal[i])
+    # rounds where rev[t] pointed past the end of a short list are refilled in order
+    seen = set(out)
+    out += [s for s in bal if s not in seen]
+    return tuple(out)
 
 
 class SlotError(RuntimeError):
@@ -107,6 +128,8 @@ class DecodeScheduler:
         if self.mode == "fused":
             if self.row_order == "balanced":
                 order = balanced_order(act, self.live)
+            elif self.row_order == "interleaved":
+                order = interleaved_order(act, self.live)
             else:
                 order = mrg + app if self.merge_first else tuple(act)
             return StepPlan(order, app, mrg, ("fused", len(act)))

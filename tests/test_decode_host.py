@@ -153,3 +153,20 @@ def test_mirror_matches_steps_since_admission_mod_M(mode, seed):
                 since[x] += 1
         for x in s.active:
             assert s.live[x] == since[x] % M
+
+
+def test_interleaved_order_is_a_balanced_permutation():
+    """The interleaved row order keeps the balanced order's per-XCD shares (each XCD's
+    rows are every eighth row of the balanced order) and only permutes their dispatch
+    order; any row count works."""
+    import numpy as np
+    from paper_2608_15533_amd.scheduler import interleaved_order
+    rng = np.random.default_rng(3)
+    for n in (256, 37, 8, 1):
+        live = rng.integers(0, 16, size=n)
+        o = interleaved_order(range(n), live)
+        assert sorted(o) == list(range(n))
+    live = rng.integers(0, 16, size=256)
+    o, b = interleaved_order(range(256), live), balanced_order(range(256), live)
+    for x in range(8):
+        assert sorted(o[x::8]) == sorted(b[x::8])
