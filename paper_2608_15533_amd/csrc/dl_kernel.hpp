@@ -757,7 +757,9 @@ void deltalog_kernel(KParams p) {
     RawRun<float, (DL == 1) ? 8 : RPL> ln_raw{};
     float ln0 = 0.f;
     bool next_ready = false;                      // uniform
-    for (int i0 = 0; i0 < L; i0 += CF::EPP) {     // uniform trip count
+    // The short STEP/MERGE build runs with C <= EPP: at most one pass, compiled as such.
+    const int passes_end = CF::CAP_ONE_PASS ? min(L, 1) : L;
+    for (int i0 = 0; i0 < passes_end; i0 += CF::EPP) {   // uniform trip count
       const int i = i0 + e_;
       const int chunk = i0 / CF::CH;
       const bool stage = CF::MERGES_LOG && merging && chunk < kKtChunks;
@@ -872,11 +874,13 @@ void deltalog_kernel(KParams p) {
         ov = fma4(s_gq[rg + NRG], up1, ov);
         if (stage_u && rg + NRG < CF::CH) s_u[(rg + NRG) * NCG + cg] = up1;
       }
-      for (int i = rg + (DL_PREFETCH_U ? 2 * NRG : 0); i < L; i += NRG) {
-        const float4 uv = ld4(Ub + size_t(i) * DV + 4 * cg);
-        if constexpr (CF::NEEDS_C) cv = fma4(s_gk[i], uv, cv);
-        ov = fma4(s_gq[i], uv, ov);
-        if (stage_u && i < CF::CH) s_u[i * NCG + cg] = uv;
+      if constexpr (!(CF::CAP_ONE_PASS && DL_PREFETCH_U && 2 * NRG >= CF::CH)) {
+        for (int i = rg + (DL_PREFETCH_U ? 2 * NRG : 0); i < L; i += NRG) {
+          const float4 uv = ld4(Ub + size_t(i) * DV + 4 * cg);
+          if constexpr (CF::NEEDS_C) cv = fma4(s_gk[i], uv, cv);
+          ov = fma4(s_gq[i], uv, ov);
+          if (stage_u && i < CF::CH) s_u[i * NCG + cg] = uv;
+        }
       }
     }
     // Rows of one column group live in lanes NCG apart inside a wave, then across waves.
@@ -1011,7 +1015,10 @@ void deltalog_kernel(KParams p) {
       // per-key head loads them after the barrier (recently read: L2 hits).
       constexpr bool kKtEarly = kUEarly && CF::NSTAGE == 1 && (DL == 1 || RPT <= 8);
       if (kKtEarly && first_kt < L) load_kt(first_kt);
-      for (int i0 = 0; i0 < L; i0 += CF::CH) {     // uniform trip count
+      // One chunk in the short STEP build (the MERGE kernel keeps the general loop: its
+      // registers come out lower that way, 112 against 140 for a 128² per-key head).
+      const int chunks_end = (CF::CAP_ONE_PASS && MODE == M_STEP) ? min(L, 1) : L;
+      for (int i0 = 0; i0 < chunks_end; i0 += CF::CH) {         // uniform trip count
         const int chunk = i0 / CF::CH;
         const int n = min(CF::CH, L - i0);
         const bool kt_staged = CF::REPLAYS && chunk < CF::NSTAGE;
@@ -1031,6 +1038,7 @@ void deltalog_kernel(KParams p) {
           }
           __syncthreads();
         }
+#pragma unroll 1
         for (int ii = 0; ii < n; ii += 4) {          // zero-padded to a multiple of 4
           const float4 u0 = s_u[(ii + 0) * NCG + cg];
           const float4 u1 = s_u[(ii + 1) * NCG + cg];
