@@ -24,7 +24,11 @@ ARCH = "gfx950"
 SOURCES = ["abi.cpp", "dl_gdn.hip", "dl_kda.hip", "dl_rwkv6.hip", "dl_linattn.hip",
            "dl_retnet.hip", "dl_gla.hip", "dl_noalloc.hip"]
 
-DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+# No packed-fp32 instructions; MFMA accumulators in ordinary VGPRs (the merge's MFMA
+# contraction accumulates into the state tile's own registers: AGPR accumulators would
+# add 64 registers per lane and halve the occupancy).
+DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+                "-mllvm", "-amdgpu-mfma-vgpr-form=1"]
 
 
 def hipcc():
@@ -91,4 +95,13 @@ def build_c_example(verbose=False):
 
 
 if __name__ == "__main__":
-    build(verbose=True, extra_flags=sys.argv[1:])
+    # python -m paper_2608_15533_amd.build [--out DIR] [hipcc flags, e.g. -DDL_MFMA_MERGE=1]
+    # With --out the library (and its objects) go to DIR instead of the package: a build
+    # variant that DELTALOG_LIB=DIR/libdeltalog.so selects at load time.
+    args = sys.argv[1:]
+    if args[:1] == ["--out"]:
+        out = os.path.abspath(args[1])
+        args = args[2:]
+        BUILD_DIR = os.path.join(out, "obj")
+        LIB = os.path.join(out, "libdeltalog.so")
+    build(verbose=True, extra_flags=args)

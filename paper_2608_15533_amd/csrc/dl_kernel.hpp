@@ -206,6 +206,17 @@ __device__ __forceinline__ float dl_exp(float x) { return __expf(x); }
 #ifndef DL_U_EARLY
 #define DL_U_EARLY 1
 #endif
+// The merge's rank-(L+1) contraction (Eq. 6) on the matrix cores (1: fp32 MFMA, twice
+// the rate of plain fp32 FMAs; 128-column heads) or on the vector ALUs (0).  See
+// MfmaMerge below.  Off: on MI355X the MFMA build wrote a wrong merged tile now and then
+// (about one (slot, head) in 10^5 merges, always the same accumulator register in lanes
+// 12-15 of each 16-lane row), which the VALU build never did in the same runs.
+#ifndef DL_MFMA_MERGE
+#define DL_MFMA_MERGE 0
+#endif
+#ifndef DL_MFMA_DRAIN
+#define DL_MFMA_DRAIN 1
+#endif
 // Issue order of the log entries relative to the state tile (see the kernel).
 #ifndef DL_LOG_FIRST
 #define DL_LOG_FIRST 0
@@ -500,6 +511,72 @@ struct Cfg {
   static_assert(LPE <= 16 && 16 % LPE == 0, "an entry's lanes share one 16-lane row");
   static_assert(NT == threads_per_head(DK, DV), "launch bound must match the layout");
   static_assert(!(BONUS && DL == 1), "the bonus readout is only defined with per-key decay");
+};
+
+// ------------------------------------------------------------ MFMA merge contraction
+// The merge adds sum_i K~_i U_i^T to the decayed tile (Eq. 6), a product of a dk x n and
+// an n x dv matrix for a chunk of n log entries.  The tile is held row-streamed: thread
+// (rg, cg) owns rows rg + NRG j (j < RPT) and columns 4 cg .. 4 cg + 3, one 16-byte load
+// or store per row.  An fp32 MFMA leaves each lane one output column and a fixed set of
+// output rows.  Both index maps of the product are free, so they are chosen to make the
+// MFMA's output fragment the thread's own tile registers, with no data movement:
+//   * output column n of block b (b < 4) is state column 4 n + b, so the four blocks of
+//     a lane hold the four columns of its quad;
+//   * output row m is the state row that the lane holding m owns, so a lane's output
+//     rows are its own rows rg + NRG j.
+// With 128 columns (NCG = 32) a wave owns two row groups, 32 rows, and the product is
+// v_mfma_f32_32x32x2f32: lane l = 32 h + n holds output rows 8 (k / 4) + 4 h + k % 4
+// (k < 16), i.e. row group 2 w + h, row j = k.  The A operand (K~) of lane (h, n) is entry
+// h of the K-step at the row whose output lane n owns; the B operand (U) is entry h at
+// column 4 n + b, i.e. component b of the U quad of column group n = cg.  Heads with 64
+// columns keep the VALU contraction.  The accumulators must be ordinary VGPRs (the
+// build's -amdgpu-mfma-vgpr-form): AGPR accumulators would add 64 registers per lane.
+template <int NCG, int RPT>
+struct MfmaMerge {                                // unused: VALU contraction
+  static constexpr int KS = 2, NMB = 1;
+  static __device__ __forceinline__ int row_of(int, int, int, int) { return 0; }
+  __device__ __forceinline__ void from_rows(const float4*) {}
+  __device__ __forceinline__ void to_rows(float4*) const {}
+  __device__ __forceinline__ void step(const float*, float4) {}
+  __device__ __forceinline__ void drain() {}
+};
+
+template <int RPT>
+struct MfmaMerge<32, RPT> {                       // v_mfma_f32_32x32x2f32
+  static_assert(RPT == 16, "a 32-row block is the two row groups of a wave");
+  using V = float __attribute__((ext_vector_type(16)));
+  static constexpr int KS = 2;                    // log entries per MFMA
+  static constexpr int NMB = 1;                   // row blocks per wave
+  V acc[4];
+  // State row of output row m of the wave's block (row group 2w + (m / 4) % 2, row
+  // 4 (m / 8) + m % 4 of it).
+  static __device__ __forceinline__ int row_of(int w, int /*mb*/, int m, int NRG) {
+    return 2 * w + (m / 4) % 2 + NRG * (4 * (m / 8) + m % 4);
+  }
+  __device__ __forceinline__ void from_rows(const float4* t) {
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      acc[0][j] = t[j].x; acc[1][j] = t[j].y; acc[2][j] = t[j].z; acc[3][j] = t[j].w;
+    }
+  }
+  __device__ __forceinline__ void to_rows(float4* t) const {
+#pragma unroll
+    for (int j = 0; j < 16; ++j) t[j] = make_float4(acc[0][j], acc[1][j], acc[2][j], acc[3][j]);
+  }
+  __device__ __forceinline__ void step(const float* a, float4 b) {
+    acc[0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[0], b.x, acc[0], 0, 0, 0);
+    acc[1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[0], b.y, acc[1], 0, 0, 0);
+    acc[2] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[0], b.z, acc[2], 0, 0, 0);
+    acc[3] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[0], b.w, acc[3], 0, 0, 0);
+  }
+  // Wait states between the last MFMA and the first VALU read of its results, on top
+  // of those the compiler inserts.
+  __device__ __forceinline__ void drain() {
+#if DL_MFMA_DRAIN
+    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7"
+                 : "+v"(acc[0]), "+v"(acc[1]), "+v"(acc[2]), "+v"(acc[3]));
+#endif
+  }
 };
 
 // U_log holds the delta rule's corrected values in fp32, and exact copies of v (in the
@@ -1018,6 +1095,17 @@ void deltalog_kernel(KParams p) {
       // One chunk in the short STEP build (the MERGE kernel keeps the general loop: its
       // registers come out lower that way, 112 against 140 for a 128² per-key head).
       const int chunks_end = (CF::CAP_ONE_PASS && MODE == M_STEP) ? min(L, 1) : L;
+      using MM = MfmaMerge<NCG, RPT>;
+      constexpr bool kMfma = DL_MFMA_MERGE && NCG == 32;   // 128-column heads
+      MM mm;
+      int a_off[MM::NMB];                           // LDS offset of this lane's A row, per block
+      const int kq = (tid % 64) / NCG;              // the lane's entry within a K-step
+      if constexpr (kMfma) {
+#pragma unroll
+        for (int mb = 0; mb < MM::NMB; ++mb)
+          a_off[mb] = CF::kt_row(MM::row_of(tid / 64, mb, cg, NRG)) * CF::KTS + kq;
+        mm.from_rows(m);
+      }
       for (int i0 = 0; i0 < chunks_end; i0 += CF::CH) {         // uniform trip count
         const int chunk = i0 / CF::CH;
         const int n = min(CF::CH, L - i0);
@@ -1038,6 +1126,28 @@ void deltalog_kernel(KParams p) {
           }
           __syncthreads();
         }
+        if constexpr (kMfma) {
+          // The operands of the whole chunk are read from LDS up front (the compiler
+          // spreads the reads over the first MFMAs).  The chunk is zero-padded to CH
+          // entries (both K~ and U); the second half is skipped when the chunk holds at
+          // most CH / 2 entries.
+          constexpr int NKS = CF::CH / MM::KS;
+          float a[NKS][MM::NMB];
+          float4 b[NKS];
+#pragma unroll
+          for (int k = 0; k < NKS; ++k) {
+#pragma unroll
+            for (int mb = 0; mb < MM::NMB; ++mb) a[k][mb] = kt[a_off[mb] + k * MM::KS];
+            b[k] = s_u[(k * MM::KS + kq) * NCG + cg];
+          }
+#pragma unroll
+          for (int k = 0; k < NKS / 2; ++k) mm.step(a[k], b[k]);
+          if (n > CF::CH / 2) {
+#pragma unroll
+            for (int k = NKS / 2; k < NKS; ++k) mm.step(a[k], b[k]);
+          }
+          continue;
+        }
 #pragma unroll 1
         for (int ii = 0; ii < n; ii += 4) {          // zero-padded to a multiple of 4
           const float4 u0 = s_u[(ii + 0) * NCG + cg];
@@ -1054,6 +1164,10 @@ void deltalog_kernel(KParams p) {
             m[j] = fma4(k4.w, u3, m[j]);
           }
         }
+      }
+      if constexpr (kMfma) {
+        mm.drain();
+        mm.to_rows(m);
       }
     }
 #pragma unroll
