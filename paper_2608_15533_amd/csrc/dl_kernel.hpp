@@ -207,12 +207,10 @@ __device__ __forceinline__ float dl_exp(float x) { return __expf(x); }
 #define DL_U_EARLY 1
 #endif
 // The merge's rank-(L+1) contraction (Eq. 6) on the matrix cores (1: fp32 MFMA, twice
-// the rate of plain fp32 FMAs; 128-column heads) or on the vector ALUs (0).  See
-// MfmaMerge below.  Off: on MI355X the MFMA build wrote a wrong merged tile now and then
-// (about one (slot, head) in 10^5 merges, always the same accumulator register in lanes
-// 12-15 of each 16-lane row), which the VALU build never did in the same runs.
+// the rate of plain fp32 FMAs; 128-column heads with an fp32 state) or on the vector
+// ALUs (0).  See MfmaMerge below.
 #ifndef DL_MFMA_MERGE
-#define DL_MFMA_MERGE 0
+#define DL_MFMA_MERGE 1
 #endif
 #ifndef DL_MFMA_DRAIN
 #define DL_MFMA_DRAIN 1
@@ -263,6 +261,14 @@ template <> struct StateQuad<float> {
                      __float_as_uint(v.w)};
     __builtin_amdgcn_raw_buffer_store_b128(x, r, voff, soff, kStateCachePolicy);
   }
+  // The materialised rows at the end of a kernel: the row registers are the store data
+  // and nothing writes them afterwards.
+  template <int N>
+  static __device__ __forceinline__ void store_rows(__amdgpu_buffer_rsrc_t r, uint32_t voff,
+                                                    uint32_t row_block, const float4 (&m)[N]) {
+#pragma unroll
+    for (int j = 0; j < N; ++j) store(r, voff, j * row_block, m[j]);
+  }
 };
 template <> struct StateQuad<uint16_t> {
   uint2 w;
@@ -279,6 +285,27 @@ template <> struct StateQuad<uint16_t> {
     typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
     const u32x2 x = {bf16_rne(v.x) | (bf16_rne(v.y) << 16), bf16_rne(v.z) | (bf16_rne(v.w) << 16)};
     __builtin_amdgcn_raw_buffer_store_b64(x, r, voff, soff, kStateCachePolicy);
+  }
+  // The materialised rows at the end of a kernel, rounded into registers of their own
+  // that stay allocated until the last store has issued, so that no store's data
+  // registers are rewritten right behind it (the fp32 MFMA build showed that a 16-byte
+  // state store can then write the new value in some lanes).
+  template <int N>
+  static __device__ __forceinline__ void store_rows(__amdgpu_buffer_rsrc_t r, uint32_t voff,
+                                                    uint32_t row_block, const float4 (&m)[N]) {
+    typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+    u32x2 x[N];
+#pragma unroll
+    for (int j = 0; j < N; ++j) {
+      x[j] = u32x2{bf16_rne(m[j].x) | (bf16_rne(m[j].y) << 16),
+                   bf16_rne(m[j].z) | (bf16_rne(m[j].w) << 16)};
+      asm volatile("" : "+v"(x[j]));
+    }
+#pragma unroll
+    for (int j = 0; j < N; ++j)
+      __builtin_amdgcn_raw_buffer_store_b64(x[j], r, voff, j * row_block, kStateCachePolicy);
+#pragma unroll
+    for (int j = 0; j < N; ++j) asm volatile("" ::"v"(x[j]));
   }
 };
 
@@ -539,6 +566,7 @@ struct MfmaMerge {                                // unused: VALU contraction
   __device__ __forceinline__ void to_rows(float4*) const {}
   __device__ __forceinline__ void step(const float*, float4) {}
   __device__ __forceinline__ void drain() {}
+  __device__ __forceinline__ void store_rows(__amdgpu_buffer_rsrc_t, uint32_t, uint32_t) const {}
 };
 
 template <int RPT>
@@ -568,6 +596,28 @@ struct MfmaMerge<32, RPT> {                       // v_mfma_f32_32x32x2f32
     acc[1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[0], b.y, acc[1], 0, 0, 0);
     acc[2] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[0], b.z, acc[2], 0, 0, 0);
     acc[3] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[0], b.w, acc[3], 0, 0, 0);
+  }
+  // The tile's rows from the accumulators (component b of row j of the lane's quad is
+  // register j of block b), one 16-byte store per row.  Every row is gathered into
+  // registers of its own, and all of them stay allocated until the last store has issued:
+  // gathered into one reused set of four registers, each row's registers were rewritten
+  // right behind its store, and on the GPU that store then wrote the next row's value in
+  // lanes 12-15 of each 16-lane row now and then.
+  __device__ __forceinline__ void store_rows(__amdgpu_buffer_rsrc_t r, uint32_t voff,
+                                             uint32_t row_block) const {
+    typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+    u32x4 x[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      x[j] = u32x4{__float_as_uint(acc[0][j]), __float_as_uint(acc[1][j]),
+                   __float_as_uint(acc[2][j]), __float_as_uint(acc[3][j])};
+      asm volatile("" : "+v"(x[j]));
+    }
+#pragma unroll
+    for (int j = 0; j < 16; ++j)
+      __builtin_amdgcn_raw_buffer_store_b128(x[j], r, voff, j * row_block, kStateCachePolicy);
+#pragma unroll
+    for (int j = 0; j < 16; ++j) asm volatile("" ::"v"(x[j]));
   }
   // Wait states between the last MFMA and the first VALU read of its results, on top
   // of those the compiler inserts.
@@ -1037,6 +1087,11 @@ void deltalog_kernel(KParams p) {
       m[j] = s_em[r] * t[j].get();
       if constexpr (CF::HAS_TOKEN) m[j] = fma4(s_kf[CF::cp_pos_group(rg, j)], bv, m[j]);
     }
+    // The contraction on MFMA: 128-column heads with an fp32 state (the rows are stored
+    // straight from the accumulators).
+    using MM = MfmaMerge<NCG, RPT>;
+    constexpr bool kMfma = DL_MFMA_MERGE && NCG == 32 && sizeof(TS) == 4 && CF::MERGES_LOG;
+    MM mm;
     if constexpr (CF::MERGES_LOG) {
       // Log values of chunk c >= 1 (chunk 0 was staged by the replay): UPT quads per
       // thread, loaded before the previous chunk's contraction where DL_U_EARLY.
@@ -1095,9 +1150,6 @@ void deltalog_kernel(KParams p) {
       // One chunk in the short STEP build (the MERGE kernel keeps the general loop: its
       // registers come out lower that way, 112 against 140 for a 128² per-key head).
       const int chunks_end = (CF::CAP_ONE_PASS && MODE == M_STEP) ? min(L, 1) : L;
-      using MM = MfmaMerge<NCG, RPT>;
-      constexpr bool kMfma = DL_MFMA_MERGE && NCG == 32;   // 128-column heads
-      MM mm;
       int a_off[MM::NMB];                           // LDS offset of this lane's A row, per block
       const int kq = (tid % 64) / NCG;              // the lane's entry within a K-step
       if constexpr (kMfma) {
@@ -1165,15 +1217,17 @@ void deltalog_kernel(KParams p) {
           }
         }
       }
-      if constexpr (kMfma) {
-        mm.drain();
-        mm.to_rows(m);
-      }
+      if constexpr (kMfma) mm.drain();
     }
-#pragma unroll
-    for (int j = 0; j < RPT; ++j) StateQuad<TS>::store(srs, toff, j * kRowBlock, m[j]);
+    // The live length is written before the rows, so that no register is written
+    // behind the state stores.
     if constexpr (CF::HAS_LOG) {
       if (tid == 0) p.len[sh] = 0;                 // the cumulative log-decay restarts at 0
+    }
+    if constexpr (kMfma) {
+      mm.store_rows(srs, toff, kRowBlock);
+    } else {
+      StateQuad<TS>::store_rows(srs, toff, kRowBlock, m);
     }
   }
 }
