@@ -286,26 +286,12 @@ template <> struct StateQuad<uint16_t> {
     const u32x2 x = {bf16_rne(v.x) | (bf16_rne(v.y) << 16), bf16_rne(v.z) | (bf16_rne(v.w) << 16)};
     __builtin_amdgcn_raw_buffer_store_b64(x, r, voff, soff, kStateCachePolicy);
   }
-  // The materialised rows at the end of a kernel, rounded into registers of their own
-  // that stay allocated until the last store has issued, so that no store's data
-  // registers are rewritten right behind it (the fp32 MFMA build showed that a 16-byte
-  // state store can then write the new value in some lanes).
+  // The materialised rows at the end of a kernel.
   template <int N>
   static __device__ __forceinline__ void store_rows(__amdgpu_buffer_rsrc_t r, uint32_t voff,
                                                     uint32_t row_block, const float4 (&m)[N]) {
-    typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
-    u32x2 x[N];
 #pragma unroll
-    for (int j = 0; j < N; ++j) {
-      x[j] = u32x2{bf16_rne(m[j].x) | (bf16_rne(m[j].y) << 16),
-                   bf16_rne(m[j].z) | (bf16_rne(m[j].w) << 16)};
-      asm volatile("" : "+v"(x[j]));
-    }
-#pragma unroll
-    for (int j = 0; j < N; ++j)
-      __builtin_amdgcn_raw_buffer_store_b64(x[j], r, voff, j * row_block, kStateCachePolicy);
-#pragma unroll
-    for (int j = 0; j < N; ++j) asm volatile("" ::"v"(x[j]));
+    for (int j = 0; j < N; ++j) store(r, voff, j * row_block, m[j]);
   }
 };
 
