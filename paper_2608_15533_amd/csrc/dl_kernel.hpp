@@ -207,10 +207,13 @@ __device__ __forceinline__ float dl_exp(float x) { return __expf(x); }
 #define DL_U_EARLY 1
 #endif
 // The merge's rank-(L+1) contraction (Eq. 6) on the matrix cores (1: fp32 MFMA, twice
-// the rate of plain fp32 FMAs; 128-column heads with an fp32 state) or on the vector
-// ALUs (0).  See MfmaMerge below.
+// the rate of plain fp32 FMAs; 128-column heads) or on the vector ALUs (0).  See
+// MfmaMerge below.  DL_MFMA_MERGE_BF16_STATE = 0 keeps a bf16 state on the VALU path.
 #ifndef DL_MFMA_MERGE
 #define DL_MFMA_MERGE 1
+#endif
+#ifndef DL_MFMA_MERGE_BF16_STATE
+#define DL_MFMA_MERGE_BF16_STATE 1
 #endif
 #ifndef DL_MFMA_DRAIN
 #define DL_MFMA_DRAIN 1
@@ -1073,10 +1076,11 @@ void deltalog_kernel(KParams p) {
       m[j] = s_em[r] * t[j].get();
       if constexpr (CF::HAS_TOKEN) m[j] = fma4(s_kf[CF::cp_pos_group(rg, j)], bv, m[j]);
     }
-    // The contraction on MFMA: 128-column heads with an fp32 state (the rows are stored
-    // straight from the accumulators).
+    // The contraction on MFMA for 128-column heads.  An fp32 state is stored straight
+    // from the accumulators; a bf16 state is rounded from them.
     using MM = MfmaMerge<NCG, RPT>;
-    constexpr bool kMfma = DL_MFMA_MERGE && NCG == 32 && sizeof(TS) == 4 && CF::MERGES_LOG;
+    constexpr bool kMfma = DL_MFMA_MERGE && NCG == 32 && CF::MERGES_LOG &&
+                           (sizeof(TS) == 4 || DL_MFMA_MERGE_BF16_STATE);
     MM mm;
     if constexpr (CF::MERGES_LOG) {
       // Log values of chunk c >= 1 (chunk 0 was staged by the replay): UPT quads per
@@ -1210,8 +1214,11 @@ void deltalog_kernel(KParams p) {
     if constexpr (CF::HAS_LOG) {
       if (tid == 0) p.len[sh] = 0;                 // the cumulative log-decay restarts at 0
     }
-    if constexpr (kMfma) {
+    if constexpr (kMfma && sizeof(TS) == 4) {
       mm.store_rows(srs, toff, kRowBlock);
+    } else if constexpr (kMfma) {
+      mm.to_rows(m);
+      StateQuad<TS>::store_rows(srs, toff, kRowBlock, m);
     } else {
       StateQuad<TS>::store_rows(srs, toff, kRowBlock, m);
     }
