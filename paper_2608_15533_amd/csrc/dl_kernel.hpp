@@ -884,15 +884,28 @@ void deltalog_kernel(KParams p) {
       const bool from_next = next_ready;
       const bool from_first = kFirstPrefetched && i0 == 0;
       constexpr bool kNextSnap = kNext == 1;      // snapshots prefetched too
-      if (i < L && !from_next && !from_first) {
-        ld_run<RPL>(Kb + size_t(i) * DK + c_ * RPL, kr);
-      }
-      if (i < L && !from_first && !(from_next && kNextSnap)) {
+      // This pass's own loads, issued together and unconditionally (lanes past the live
+      // length re-read entry L-1, unused): a load under a per-lane condition is waited
+      // for at the condition's end, which would serialise the key and snapshot round
+      // trips.
+      const bool keys_here = !from_next && !from_first;                   // uniform
+      const bool snaps_here = !from_first && !(from_next && kNextSnap);
+      const int ic = min(i, L - 1);
+      RawRun<TIN, RPL> kc_raw{};
+      RawRun<float, (DL == 1) ? 8 : RPL> lc_raw{};
+      float lc0 = 0.f;
+      if (keys_here) kc_raw.load(Kb + size_t(ic) * DK + c_ * RPL);
+      if (snaps_here) {
         if constexpr (DL == 1) {
-          if constexpr (CF::DECAY) lr_[0] = Lb[size_t(i) * LS];
+          if constexpr (CF::DECAY) lc0 = Lb[size_t(ic) * LS];
         } else {
-          ld_run<RPL>(Lb + size_t(i) * DK + c_ * RPL, lr_);
+          lc_raw.load(Lb + size_t(ic) * DK + c_ * RPL);
         }
+      }
+      if (keys_here) kc_raw.get(kr);
+      if (snaps_here) {
+        if constexpr (DL == 1) lr_[0] = lc0;
+        else lc_raw.get(lr_);
       }
       if (from_next) {
         kn_raw.get(kr);
