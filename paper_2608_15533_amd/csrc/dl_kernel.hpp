@@ -206,6 +206,13 @@ __device__ __forceinline__ float dl_exp(float x) { return __expf(x); }
 #ifndef DL_U_EARLY
 #define DL_U_EARLY 1
 #endif
+//   DL_REPLAY_PAIRS        replay the log values past the first two per row group two
+//                          at a time, with both loads issued before either is used
+//                          (delta-rule operators: elsewhere the second value's registers
+//                          cost a wave per SIMD).
+#ifndef DL_REPLAY_PAIRS
+#define DL_REPLAY_PAIRS 1
+#endif
 // The merge's rank-(L+1) contraction (Eq. 6) on the matrix cores (1: fp32 MFMA, twice
 // the rate of plain fp32 FMAs; 128-column heads) or on the vector ALUs (0).  See
 // MfmaMerge below.  DL_MFMA_MERGE_BF16_STATE = 0 keeps a bf16 state on the VALU path.
@@ -1003,8 +1010,26 @@ void deltalog_kernel(KParams p) {
         ov = fma4(s_gq[rg + NRG], up1, ov);
         if (stage_u && rg + NRG < CF::CH) s_u[(rg + NRG) * NCG + cg] = up1;
       }
-      if constexpr (!(CF::CAP_ONE_PASS && DL_PREFETCH_U && 2 * NRG >= CF::CH)) {
-        for (int i = rg + (DL_PREFETCH_U ? 2 * NRG : 0); i < L; i += NRG) {
+      constexpr int kFirstLater = DL_PREFETCH_U ? 2 * NRG : 0;   // first entry replayed here
+      if constexpr (LONG && DL_REPLAY_PAIRS && CF::DELTA && kFirstLater >= CF::CH) {
+        // The later values two rows of entries at a time, on a loop bound that is uniform
+        // over the workgroup: both loads are issued before either is used.  Lanes past
+        // the live length re-read entry L-1 (a finite value) with a zero coefficient, so
+        // no load waits at the end of a per-lane condition.
+        for (int base = kFirstLater; base < L; base += 2 * NRG) {
+          const int i0 = base + rg, i1 = base + NRG + rg;
+          const int j0 = min(i0, L - 1), j1 = min(i1, L - 1);
+          const float4 u0 = ld4(Ub + size_t(j0) * DV + 4 * cg);
+          const float4 u1 = ld4(Ub + size_t(j1) * DV + 4 * cg);
+          if constexpr (CF::NEEDS_C) {
+            cv = fma4(i0 < L ? s_gk[j0] : 0.f, u0, cv);
+            cv = fma4(i1 < L ? s_gk[j1] : 0.f, u1, cv);
+          }
+          ov = fma4(i0 < L ? s_gq[j0] : 0.f, u0, ov);
+          ov = fma4(i1 < L ? s_gq[j1] : 0.f, u1, ov);
+        }
+      } else if constexpr (!(CF::CAP_ONE_PASS && DL_PREFETCH_U && 2 * NRG >= CF::CH)) {
+        for (int i = rg + kFirstLater; i < L; i += NRG) {
           const float4 uv = ld4(Ub + size_t(i) * DV + 4 * cg);
           if constexpr (CF::NEEDS_C) cv = fma4(s_gk[i], uv, cv);
           ov = fma4(s_gq[i], uv, ov);
