@@ -207,9 +207,7 @@ __device__ __forceinline__ float dl_exp(float x) { return __expf(x); }
 #define DL_U_EARLY 1
 #endif
 //   DL_REPLAY_PAIRS        replay the log values past the first two per row group two
-//                          at a time, with both loads issued before either is used
-//                          (delta-rule operators: elsewhere the second value's registers
-//                          cost a wave per SIMD).
+//                          at a time, with both loads issued before either is used.
 #ifndef DL_REPLAY_PAIRS
 #define DL_REPLAY_PAIRS 1
 #endif
@@ -635,10 +633,19 @@ struct UType { using type = std::conditional_t<OpTraits<OP>::DELTA, float, TIN>;
 #ifndef DL_SMALL_HEAD_WAVES
 #define DL_SMALL_HEAD_WAVES 6
 #endif
-constexpr int waves_target(int dk, int dv) {
-  return DL_WAVES_PER_EU > 0 ? DL_WAVES_PER_EU : ((dk == 64 && dv == 64) ? DL_SMALL_HEAD_WAVES : 1);
+// The long build of 128^2 heads with bf16 activations is held to 4 waves per SIMD (128
+// registers), the occupancy its short build has.
+#ifndef DL_LONG_WAVES
+#define DL_LONG_WAVES 4
+#endif
+constexpr int waves_target(int dk, int dv, bool long_build, int in_bytes) {
+  return DL_WAVES_PER_EU > 0 ? DL_WAVES_PER_EU
+         : (dk == 64 && dv == 64) ? DL_SMALL_HEAD_WAVES
+         : (long_build && dk == 128 && dv == 128 && in_bytes == 2) ? DL_LONG_WAVES
+                                                                    : 1;
 }
-#define DL_OCCUPANCY __attribute__((amdgpu_waves_per_eu(waves_target(DK, DV))))
+#define DL_OCCUPANCY \
+  __attribute__((amdgpu_waves_per_eu(waves_target(DK, DV, LONG, int(sizeof(TIN))))))
 
 // ------------------------------------------------------------------ the kernel
 // Every global load a workgroup needs is issued before its first barrier: the token
@@ -1011,7 +1018,7 @@ void deltalog_kernel(KParams p) {
         if (stage_u && rg + NRG < CF::CH) s_u[(rg + NRG) * NCG + cg] = up1;
       }
       constexpr int kFirstLater = DL_PREFETCH_U ? 2 * NRG : 0;   // first entry replayed here
-      if constexpr (LONG && DL_REPLAY_PAIRS && CF::DELTA && kFirstLater >= CF::CH) {
+      if constexpr (LONG && DL_REPLAY_PAIRS && kFirstLater >= CF::CH) {
         // The later values two rows of entries at a time, on a loop bound that is uniform
         // over the workgroup: both loads are issued before either is used.  Lanes past
         // the live length re-read entry L-1 (a finite value) with a zero coefficient, so
@@ -1019,13 +1026,14 @@ void deltalog_kernel(KParams p) {
         for (int base = kFirstLater; base < L; base += 2 * NRG) {
           const int i0 = base + rg, i1 = base + NRG + rg;
           const int j0 = min(i0, L - 1), j1 = min(i1, L - 1);
-          const float4 u0 = ld4(Ub + size_t(j0) * DV + 4 * cg);
-          const float4 u1 = ld4(Ub + size_t(j1) * DV + 4 * cg);
-          if constexpr (CF::NEEDS_C) {
-            cv = fma4(i0 < L ? s_gk[j0] : 0.f, u0, cv);
-            cv = fma4(i1 < L ? s_gk[j1] : 0.f, u1, cv);
-          }
+          Raw4<TU> r0, r1;                        // (bf16 values widened one at a time)
+          r0.load(Ub + size_t(j0) * DV + 4 * cg);
+          r1.load(Ub + size_t(j1) * DV + 4 * cg);
+          const float4 u0 = r0.get();
+          if constexpr (CF::NEEDS_C) cv = fma4(i0 < L ? s_gk[j0] : 0.f, u0, cv);
           ov = fma4(i0 < L ? s_gq[j0] : 0.f, u0, ov);
+          const float4 u1 = r1.get();
+          if constexpr (CF::NEEDS_C) cv = fma4(i1 < L ? s_gk[j1] : 0.f, u1, cv);
           ov = fma4(i1 < L ? s_gq[j1] : 0.f, u1, ov);
         }
       } else if constexpr (!(CF::CAP_ONE_PASS && DL_PREFETCH_U && 2 * NRG >= CF::CH)) {
