@@ -1133,11 +1133,24 @@ void deltalog_kernel(KParams p) {
       // thread, loaded before the previous chunk's contraction where DL_U_EARLY.
       constexpr int UPT = CF::UPT;
       float4 ur[UPT];
+      // Loaded unconditionally (entries past the live length re-read entry L-1) and
+      // zeroed when staged: a load under a per-lane condition would be waited for at
+      // once.
+      Raw4<TU> ur_raw[UPT];
+      int u_c0 = 0;
       auto load_u = [&](int c0) {
+        u_c0 = c0;
 #pragma unroll
         for (int k = 0; k < UPT; ++k) {
           const int x = tid + k * NT, ii = x / NCG, c4 = x % NCG;
-          ur[k] = (c0 + ii < L) ? ld4(Ub + size_t(c0 + ii) * DV + 4 * c4) : f4(0.f);
+          ur_raw[k].load(Ub + size_t(min(c0 + ii, L - 1)) * DV + 4 * c4);
+        }
+      };
+      auto widen_u = [&]() {
+#pragma unroll
+        for (int k = 0; k < UPT; ++k) {
+          const int ii = (tid + k * NT) / NCG;
+          ur[k] = (u_c0 + ii < L) ? ur_raw[k].get() : f4(0.f);
         }
       };
       const int first_global = CF::REPLAYS ? CF::CH : 0;   // first chunk whose U is loaded here
@@ -1162,9 +1175,12 @@ void deltalog_kernel(KParams p) {
       auto store_kt = [&](int c0) {
         float kv[RPL];
         kg_raw.get(kv);
-        const bool live = c0 + e_ < L;
+        // Entries past the live length (re-reads of entry L-1, finite) get a factor of
+        // 0 rather than a branch, so that neither load is moved under a per-lane
+        // condition and waited for there.
+        const float live = c0 + e_ < L ? 1.f : 0.f;
         if constexpr (DL == 1) {
-          const float w = live ? (CF::DECAY ? dl_exp(s_lm[0] - lg0) : 1.f) : 0.f;
+          const float w = live * (CF::DECAY ? dl_exp(s_lm[0] - lg0) : 1.f);
 #pragma unroll
           for (int x = 0; x < RPL; ++x) s_kt[CF::kt_row_run(c_, x) * CF::KTS + e_] = w * kv[x];
         } else {
@@ -1172,7 +1188,7 @@ void deltalog_kernel(KParams p) {
           lg_raw.get(lv);
 #pragma unroll
           for (int x = 0; x < RPL; ++x) {
-            const float w = live ? dl_exp(s_lm[CF::cp_pos_run(c_, x)] - lv[x]) : 0.f;
+            const float w = live * dl_exp(s_lm[CF::cp_pos_run(c_, x)] - lv[x]);
             s_kt[CF::kt_row_run(c_, x) * CF::KTS + e_] = w * kv[x];
           }
         }
@@ -1206,6 +1222,7 @@ void deltalog_kernel(KParams p) {
             store_kt(i0);
           }
           if (!kUEarly) load_u(i0);
+          widen_u();
 #pragma unroll
           for (int k = 0; k < UPT; ++k) s_u[tid + k * NT] = ur[k];
           if (kUEarly && i0 + CF::CH < L) {         // the next chunk, in flight meanwhile
