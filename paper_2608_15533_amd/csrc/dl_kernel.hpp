@@ -212,10 +212,14 @@ __device__ __forceinline__ float dl_exp(float x) { return __expf(x); }
 #define DL_REPLAY_PAIRS 1
 #endif
 // The merge's rank-(L+1) contraction (Eq. 6) on the matrix cores (1: fp32 MFMA, twice
-// the rate of plain fp32 FMAs; 128-column heads) or on the vector ALUs (0).  See
-// MfmaMerge below.  DL_MFMA_MERGE_BF16_STATE = 0 keeps a bf16 state on the VALU path.
+// the rate of plain fp32 FMAs) or on the vector ALUs (0).  See MfmaMerge below.
+// DL_MFMA_MERGE_64COL = 0 keeps 64-column heads, DL_MFMA_MERGE_BF16_STATE = 0 a bf16
+// state, on the VALU path.
 #ifndef DL_MFMA_MERGE
 #define DL_MFMA_MERGE 1
+#endif
+#ifndef DL_MFMA_MERGE_64COL
+#define DL_MFMA_MERGE_64COL 1
 #endif
 #ifndef DL_MFMA_MERGE_BF16_STATE
 #define DL_MFMA_MERGE_BF16_STATE 1
@@ -549,9 +553,12 @@ struct Cfg {
 // v_mfma_f32_32x32x2f32: lane l = 32 h + n holds output rows 8 (k / 4) + 4 h + k % 4
 // (k < 16), i.e. row group 2 w + h, row j = k.  The A operand (K~) of lane (h, n) is entry
 // h of the K-step at the row whose output lane n owns; the B operand (U) is entry h at
-// column 4 n + b, i.e. component b of the U quad of column group n = cg.  Heads with 64
-// columns keep the VALU contraction.  The accumulators must be ordinary VGPRs (the
-// build's -amdgpu-mfma-vgpr-form): AGPR accumulators would add 64 registers per lane.
+// column 4 n + b, i.e. component b of the U quad of column group n = cg.  With 64
+// columns (NCG = 16) a wave owns four row groups and the product is
+// v_mfma_f32_16x16x4f32 over RPT / 4 blocks of 16 rows: lane l = 16 g + n holds rows
+// 4 g + k of a block, i.e. row group 4 w + g, row j = 4 mb + k.  The accumulators must be
+// ordinary VGPRs (the build's -amdgpu-mfma-vgpr-form): AGPR accumulators would add the
+// tile's registers again.
 template <int NCG, int RPT>
 struct MfmaMerge {                                // unused: VALU contraction
   static constexpr int KS = 2, NMB = 1;
@@ -619,6 +626,73 @@ struct MfmaMerge<32, RPT> {                       // v_mfma_f32_32x32x2f32
 #if DL_MFMA_DRAIN
     asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7"
                  : "+v"(acc[0]), "+v"(acc[1]), "+v"(acc[2]), "+v"(acc[3]));
+#endif
+  }
+};
+
+template <int RPT>
+struct MfmaMerge<16, RPT> {                       // v_mfma_f32_16x16x4f32 (64 columns)
+  static_assert(RPT % 4 == 0, "16-row blocks, four rows per lane");
+  using V = float __attribute__((ext_vector_type(4)));
+  static constexpr int KS = 4;                    // log entries per MFMA
+  static constexpr int NMB = RPT / 4;             // row blocks per wave
+  V acc[NMB][4];
+  // State row of output row m of block mb: a wave owns four row groups (4 w + m / 4),
+  // and lane (g, n) holds rows 4 g + k of the block, row j = 4 mb + k of its group.
+  static __device__ __forceinline__ int row_of(int w, int mb, int m, int NRG) {
+    return 4 * w + m / 4 + NRG * (4 * mb + m % 4);
+  }
+  __device__ __forceinline__ void from_rows(const float4* t) {
+#pragma unroll
+    for (int mb = 0; mb < NMB; ++mb)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const float4 r = t[4 * mb + k];
+        acc[mb][0][k] = r.x; acc[mb][1][k] = r.y; acc[mb][2][k] = r.z; acc[mb][3][k] = r.w;
+      }
+  }
+  __device__ __forceinline__ void to_rows(float4* t) const {
+#pragma unroll
+    for (int mb = 0; mb < NMB; ++mb)
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        t[4 * mb + k] = make_float4(acc[mb][0][k], acc[mb][1][k], acc[mb][2][k], acc[mb][3][k]);
+  }
+  __device__ __forceinline__ void step(const float* a, float4 b) {
+#pragma unroll
+    for (int mb = 0; mb < NMB; ++mb) {
+      acc[mb][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mb], b.x, acc[mb][0], 0, 0, 0);
+      acc[mb][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mb], b.y, acc[mb][1], 0, 0, 0);
+      acc[mb][2] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mb], b.z, acc[mb][2], 0, 0, 0);
+      acc[mb][3] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mb], b.w, acc[mb][3], 0, 0, 0);
+    }
+  }
+  // As for 128 columns: every row in registers of its own, held until the last store.
+  __device__ __forceinline__ void store_rows(__amdgpu_buffer_rsrc_t r, uint32_t voff,
+                                             uint32_t row_block) const {
+    typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+    u32x4 x[RPT];
+#pragma unroll
+    for (int mb = 0; mb < NMB; ++mb)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int j = 4 * mb + k;
+        x[j] = u32x4{__float_as_uint(acc[mb][0][k]), __float_as_uint(acc[mb][1][k]),
+                     __float_as_uint(acc[mb][2][k]), __float_as_uint(acc[mb][3][k])};
+        asm volatile("" : "+v"(x[j]));
+      }
+#pragma unroll
+    for (int j = 0; j < RPT; ++j)
+      __builtin_amdgcn_raw_buffer_store_b128(x[j], r, voff, j * row_block, kStateCachePolicy);
+#pragma unroll
+    for (int j = 0; j < RPT; ++j) asm volatile("" ::"v"(x[j]));
+  }
+  __device__ __forceinline__ void drain() {
+#if DL_MFMA_DRAIN
+#pragma unroll
+    for (int mb = 0; mb < NMB; ++mb)
+      asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7"
+                   : "+v"(acc[mb][0]), "+v"(acc[mb][1]), "+v"(acc[mb][2]), "+v"(acc[mb][3]));
 #endif
   }
 };
@@ -1122,11 +1196,11 @@ void deltalog_kernel(KParams p) {
       m[j] = s_em[r] * t[j].get();
       if constexpr (CF::HAS_TOKEN) m[j] = fma4(s_kf[CF::cp_pos_group(rg, j)], bv, m[j]);
     }
-    // The contraction on MFMA for 128-column heads.  An fp32 state is stored straight
-    // from the accumulators; a bf16 state is rounded from them.
+    // The contraction on MFMA.  An fp32 state is stored straight from the
+    // accumulators; a bf16 state is rounded from them.
     using MM = MfmaMerge<NCG, RPT>;
-    constexpr bool kMfma = DL_MFMA_MERGE && NCG == 32 && CF::MERGES_LOG &&
-                           (sizeof(TS) == 4 || DL_MFMA_MERGE_BF16_STATE);
+    constexpr bool kMfma = DL_MFMA_MERGE && (NCG == 32 || DL_MFMA_MERGE_64COL) &&
+                           CF::MERGES_LOG && (sizeof(TS) == 4 || DL_MFMA_MERGE_BF16_STATE);
     MM mm;
     if constexpr (CF::MERGES_LOG) {
       // Log values of chunk c >= 1 (chunk 0 was staged by the replay): UPT quads per
