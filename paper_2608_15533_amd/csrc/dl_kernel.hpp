@@ -227,6 +227,15 @@ __device__ __forceinline__ float dl_exp(float x) { return __expf(x); }
 #ifndef DL_MFMA_DRAIN
 #define DL_MFMA_DRAIN 1
 #endif
+// LDS layout of the staged K~ chunk where the merge contracts on MFMA: row R starts at
+// R * S + (R / 16) * P floats (1, S and P per head shape), or at R * 20 (0; the VALU
+// contraction's float4 reads need it).  An LDS access by a wave is served 32 lanes at a
+// time over 32 banks.  The MFMA operand read has those 32 lanes on 16 or 32 different rows
+// at one entry; the staging write has them on 16 consecutive rows at two entries.  With
+// the padded layout both land in 32 different banks (with R * 20, the read met in 4 or 8).
+#ifndef DL_KT_PAD
+#define DL_KT_PAD 1
+#endif
 // Issue order of the log entries relative to the state tile (see the kernel).
 #ifndef DL_LOG_FIRST
 #define DL_LOG_FIRST 0
@@ -466,7 +475,16 @@ struct Cfg {
   static constexpr int LPE = NT / EPP;           // lanes per log entry (coefficient pass)
   static constexpr int RPL = DK / LPE;           // key rows per lane (coefficient pass)
   static constexpr int CH = 16;                  // log entries staged per merge chunk
-  static constexpr int KTS = CH + 4;             // LDS row stride of the staged K~ chunk
+  static constexpr int KTS = CH + 4;             // LDS row stride, VALU layout
+  // Padded layout (row R at R * KT_S + (R / 16) * KT_P) for the MFMA contraction; the
+  // per-shape constants are the bank-conflict-free ones for its reads and the staging
+  // writes (a 64 x 128 or 128 x 64 head keeps a 2-way conflict on the read).
+  static constexpr bool KT_PADDED = DL_KT_PAD && DL_MFMA_MERGE &&
+                                    (DV / 4 == 32 || DL_MFMA_MERGE_64COL) && DL_MFMA_MERGE_BF16_STATE;
+  static constexpr int KT_S = !KT_PADDED ? KTS : DK == DV ? 18 : 20;
+  static constexpr int KT_P = !KT_PADDED ? 0 : DV / 4 == 32 ? 1 : 2;
+  static constexpr int kt_base_c(int r) { return r * KT_S + (r / 16) * KT_P; }
+  static constexpr int KT_CHUNK = (kt_base_c(DK) + 3) / 4 * 4;   // floats per staged chunk
   // K~ chunks staged by the coefficient passes.  With per-key decay the long build keeps
   // one: the second chunk's staging slows every append (measured), and the merge stages
   // the later chunks itself, one chunk ahead.
@@ -506,6 +524,14 @@ struct Cfg {
   }
   static __device__ __forceinline__ int kt_row_run(int c, int x) {
     return DL_KT_ROW_ORDER ? x * LPE + c : c * RPL + x;
+  }
+  // LDS offset of row r of the staged chunk, and of element x of coefficient run c (with
+  // the row order above, c < LPE and LPE dividing 16 keep (x LPE + c) / 16 = x LPE / 16,
+  // so the part that depends on x is a compile-time constant).
+  static __device__ __forceinline__ int kt_base(int r) { return r * KT_S + (r >> 4) * KT_P; }
+  static __device__ __forceinline__ int kt_off_run(int c, int x) {
+    if constexpr (DL_KT_ROW_ORDER) return c * KT_S + (x * LPE * KT_S + ((x * LPE) >> 4) * KT_P);
+    else return kt_base(c * RPL + x);
   }
   // LDS position of token row r in the vectors the coefficient pass reads (the same
   // permutation as the K~ rows).
@@ -744,10 +770,10 @@ void deltalog_kernel(KParams p) {
   __shared__ float s_gq[DL_MAX_MERGE_INTERVAL];
   __shared__ float s_red[CF::NW][2][DV];
   __shared__ float s_dotw[CF::NW];
-  // K~ chunks [NSTAGE][DK][KTS]: staged by the coefficient passes where the kernel
+  // K~ chunks [NSTAGE][KT_CHUNK]: staged by the coefficient passes where the kernel
   // replays the log, else (flush) one chunk at a time from global memory
   constexpr int kKtChunks = CF::REPLAYS ? CF::NSTAGE : 1;
-  __shared__ float s_kt[CF::MERGES_LOG ? kKtChunks * DK * CF::KTS : 1];
+  __shared__ float s_kt[CF::MERGES_LOG ? kKtChunks * CF::KT_CHUNK : 1];
   __shared__ float4 s_u[CF::MERGES_LOG ? CF::CH * NCG : 1];          // U chunk  [CH][NCG]
 
   const int tid = threadIdx.x;
@@ -967,7 +993,7 @@ void deltalog_kernel(KParams p) {
       const int i = i0 + e_;
       const int chunk = i0 / CF::CH;
       const bool stage = CF::MERGES_LOG && merging && chunk < kKtChunks;
-      float* const kt = s_kt + (stage ? chunk : 0) * DK * CF::KTS;
+      float* const kt = s_kt + (stage ? chunk : 0) * CF::KT_CHUNK;
       float ak = 0.f, aq = 0.f;
       const bool from_next = next_ready;
       const bool from_first = kFirstPrefetched && i0 == 0;
@@ -1035,7 +1061,7 @@ void deltalog_kernel(KParams p) {
           if (stage) {
 #pragma unroll
             for (int x = 0; x < RPL; ++x) {
-              kt[CF::kt_row_run(c_, x) * CF::KTS + e_] = w * kr[x];
+              kt[CF::kt_off_run(c_, x) + e_] = w * kr[x];
             }
           }
         } else {
@@ -1046,14 +1072,14 @@ void deltalog_kernel(KParams p) {
             if constexpr (CF::NEEDS_C) ak = fmaf(wk, s_kf[pr], ak);
             aq = fmaf(wk, s_qf[pr], aq);
             if (stage)
-              kt[CF::kt_row_run(c_, x) * CF::KTS + e_] =
+              kt[CF::kt_off_run(c_, x) + e_] =
                   CF::BONUS ? dl_exp(s_lm[pr] - lr_[x]) * kr[x] : wk;
           }
         }
       } else if (stage) {
 #pragma unroll
         for (int x = 0; x < RPL; ++x) {
-          kt[CF::kt_row_run(c_, x) * CF::KTS + e_] = 0.f;
+          kt[CF::kt_off_run(c_, x) + e_] = 0.f;
         }
       }
       if constexpr (CF::NEEDS_C) ak = group_sum<CF::LPE>(ak);   // the delta-rule correction only
@@ -1201,6 +1227,8 @@ void deltalog_kernel(KParams p) {
     using MM = MfmaMerge<NCG, RPT>;
     constexpr bool kMfma = DL_MFMA_MERGE && (NCG == 32 || DL_MFMA_MERGE_64COL) &&
                            CF::MERGES_LOG && (sizeof(TS) == 4 || DL_MFMA_MERGE_BF16_STATE);
+    static_assert(kMfma || !CF::KT_PADDED || !CF::MERGES_LOG,
+                  "the VALU contraction reads K~ rows as float4: unpadded layout only");
     MM mm;
     if constexpr (CF::MERGES_LOG) {
       // Log values of chunk c >= 1 (chunk 0 was staged by the replay): UPT quads per
@@ -1256,14 +1284,14 @@ void deltalog_kernel(KParams p) {
         if constexpr (DL == 1) {
           const float w = live * (CF::DECAY ? dl_exp(s_lm[0] - lg0) : 1.f);
 #pragma unroll
-          for (int x = 0; x < RPL; ++x) s_kt[CF::kt_row_run(c_, x) * CF::KTS + e_] = w * kv[x];
+          for (int x = 0; x < RPL; ++x) s_kt[CF::kt_off_run(c_, x) + e_] = w * kv[x];
         } else {
           float lv[RPL];
           lg_raw.get(lv);
 #pragma unroll
           for (int x = 0; x < RPL; ++x) {
             const float w = live * dl_exp(s_lm[CF::cp_pos_run(c_, x)] - lv[x]);
-            s_kt[CF::kt_row_run(c_, x) * CF::KTS + e_] = w * kv[x];
+            s_kt[CF::kt_off_run(c_, x) + e_] = w * kv[x];
           }
         }
       };
@@ -1281,14 +1309,14 @@ void deltalog_kernel(KParams p) {
       if constexpr (kMfma) {
 #pragma unroll
         for (int mb = 0; mb < MM::NMB; ++mb)
-          a_off[mb] = CF::kt_row(MM::row_of(tid / 64, mb, cg, NRG)) * CF::KTS + kq;
+          a_off[mb] = CF::kt_base(CF::kt_row(MM::row_of(tid / 64, mb, cg, NRG))) + kq;
         mm.from_rows(m);
       }
       for (int i0 = 0; i0 < chunks_end; i0 += CF::CH) {         // uniform trip count
         const int chunk = i0 / CF::CH;
         const int n = min(CF::CH, L - i0);
         const bool kt_staged = CF::REPLAYS && chunk < CF::NSTAGE;
-        const float* const kt = s_kt + (kt_staged ? chunk : 0) * DK * CF::KTS;
+        const float* const kt = s_kt + (kt_staged ? chunk : 0) * CF::KT_CHUNK;
         __syncthreads();                            // previous chunk consumed / chunk 0 visible
         if (!(CF::REPLAYS && chunk == 0)) {
           if (!kt_staged) {                         // K~_i[r] = e^(l'_r - Lam_i,r) K_i[r]
@@ -1336,7 +1364,7 @@ void deltalog_kernel(KParams p) {
 #pragma unroll
           for (int j = 0; j < RPT; ++j) {
             const float4 k4 =
-                *reinterpret_cast<const float4*>(&kt[CF::kt_row_group(rg, j) * CF::KTS + ii]);
+                *reinterpret_cast<const float4*>(&kt[CF::kt_base(CF::kt_row_group(rg, j)) + ii]);
             m[j] = fma4(k4.x, u0, m[j]);
             m[j] = fma4(k4.y, u1, m[j]);
             m[j] = fma4(k4.z, u2, m[j]);
