@@ -195,6 +195,9 @@ __device__ __forceinline__ float dl_exp(float x) { return __expf(x); }
 //                          chunks are staged from global memory.
 //   DL_PREFETCH_NEXT_PASS  load the next coefficient pass's log keys (1: and snapshots;
 //                          2: keys only) while the current pass computes.
+//   DL_PREFETCH_NEXT_PASS_PER_KEY  the same for 128-row per-key heads with bf16
+//                          activations (0: not at all), where it fits in the 4-wave
+//                          long build.
 //   DL_U_EARLY             load the log values of the next merge chunk before
 //                          contracting the current one.
 #ifndef DL_STAGE_CHUNKS
@@ -202,6 +205,20 @@ __device__ __forceinline__ float dl_exp(float x) { return __expf(x); }
 #endif
 #ifndef DL_PREFETCH_NEXT_PASS
 #define DL_PREFETCH_NEXT_PASS 1
+#endif
+#ifndef DL_PREFETCH_NEXT_PASS_PER_KEY
+#define DL_PREFETCH_NEXT_PASS_PER_KEY 0
+#endif
+//   DL_PREFETCH_U_LATER    long builds with per-key decay, bf16 activations, an fp32
+//                          state and 8 row groups (128-row heads, whose later values
+//                          start with the second pass; the other builds would spill or
+//                          lose a wave): load
+//                          the first pair of the replay's later log values (entries
+//                          rg + 2 NRG and rg + 3 NRG)
+//                          with the first two, before the first barrier, instead of after
+//                          the coefficient passes.
+#ifndef DL_PREFETCH_U_LATER
+#define DL_PREFETCH_U_LATER 1
 #endif
 #ifndef DL_U_EARLY
 #define DL_U_EARLY 1
@@ -912,9 +929,19 @@ void deltalog_kernel(KParams p) {
     }
   }
   Raw4<TU> up0_raw{}, up1_raw{};                     // first two replay values of this row group
+  // ... and, in the long build, the next two (re-reads of entry L-1 where they are past
+  // the live length; the replay gives those a zero coefficient).
+  constexpr bool kLaterEarly = LONG && DL > 1 && sizeof(TIN) == 2 && sizeof(TS) == 4 &&
+                               CF::REPLAYS && DL_PREFETCH_U && DL_PREFETCH_U_LATER &&
+                               DL_REPLAY_PAIRS && 2 * NRG == CF::CH;
+  Raw4<TU> up2_raw{}, up3_raw{};
   if constexpr (CF::REPLAYS && DL_PREFETCH_U) {
     up0_raw.load(Up + size_t(min(rg, Lm1)) * DV + 4 * cg);
     if constexpr (CF::TWO_PER_GROUP) up1_raw.load(Up + size_t(min(rg + NRG, Lm1)) * DV + 4 * cg);
+    if constexpr (kLaterEarly) {
+      up2_raw.load(Up + size_t(min(rg + 2 * NRG, Lm1)) * DV + 4 * cg);
+      up3_raw.load(Up + size_t(min(rg + 3 * NRG, Lm1)) * DV + 4 * cg);
+    }
   }
   if constexpr (DL_LOG_FIRST) {
     sched_fence();
@@ -979,10 +1006,15 @@ void deltalog_kernel(KParams p) {
   // current pass computes.
   if constexpr (CF::REPLAYS) {
     constexpr bool kFirstPrefetched = DL_PREFETCH_KEYS && (DL == 1 || kPrefetchPerKey);
-    // The next pass is prefetched where the registers allow it at full occupancy: one
-    // log-decay per head (a scalar snapshot), or small heads; a 128-row per-key head
-    // would need 12 more registers across the pass (one wave per SIMD less).
-    constexpr int kNext = (LONG && (DL == 1 || RPT <= 8)) ? DL_PREFETCH_NEXT_PASS : 0;
+    // The next pass is prefetched where the registers allow it at the build's occupancy:
+    // one log-decay per head (a scalar snapshot), small heads, and 128² per-key heads
+    // with bf16 activations (the 4-wave long build; the bonus readout's extra registers
+    // leave room for the keys only).  With fp32 activations or other shapes a 128-row
+    // per-key head would need 12 more registers across the pass (one wave less).
+    constexpr int kNextPerKey =
+        (sizeof(TIN) == 2 && DK == 128 && DV == 128 && DL_PREFETCH_NEXT_PASS_PER_KEY)
+            ? (CF::BONUS ? 2 : DL_PREFETCH_NEXT_PASS) : 0;
+    constexpr int kNext = !LONG ? 0 : (DL == 1 || RPT <= 8) ? DL_PREFETCH_NEXT_PASS : kNextPerKey;
     RawRun<TIN, RPL> kn_raw{};
     RawRun<float, (DL == 1) ? 8 : RPL> ln_raw{};
     float ln0 = 0.f;
@@ -1123,7 +1155,19 @@ void deltalog_kernel(KParams p) {
         // over the workgroup: both loads are issued before either is used.  Lanes past
         // the live length re-read entry L-1 (a finite value) with a zero coefficient, so
         // no load waits at the end of a per-lane condition.
-        for (int base = kFirstLater; base < L; base += 2 * NRG) {
+        if constexpr (kLaterEarly) {              // the pair loaded before the first barrier
+          if (kFirstLater < L) {
+            const int i0 = kFirstLater + rg, i1 = kFirstLater + NRG + rg;
+            const int j0 = min(i0, L - 1), j1 = min(i1, L - 1);
+            const float4 u0 = up2_raw.get();
+            if constexpr (CF::NEEDS_C) cv = fma4(i0 < L ? s_gk[j0] : 0.f, u0, cv);
+            ov = fma4(i0 < L ? s_gq[j0] : 0.f, u0, ov);
+            const float4 u1 = up3_raw.get();
+            if constexpr (CF::NEEDS_C) cv = fma4(i1 < L ? s_gk[j1] : 0.f, u1, cv);
+            ov = fma4(i1 < L ? s_gq[j1] : 0.f, u1, ov);
+          }
+        }
+        for (int base = kFirstLater + (kLaterEarly ? 2 * NRG : 0); base < L; base += 2 * NRG) {
           const int i0 = base + rg, i1 = base + NRG + rg;
           const int j0 = min(i0, L - 1), j1 = min(i1, L - 1);
           Raw4<TU> r0, r1;                        // (bf16 values widened one at a time)
