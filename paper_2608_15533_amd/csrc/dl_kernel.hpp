@@ -196,8 +196,9 @@ __device__ __forceinline__ float dl_exp(float x) { return __expf(x); }
 //   DL_PREFETCH_NEXT_PASS  load the next coefficient pass's log keys (1: and snapshots;
 //                          2: keys only) while the current pass computes.
 //   DL_PREFETCH_NEXT_PASS_PER_KEY  the same for 128-row per-key heads with bf16
-//                          activations (0: not at all), where it fits in the 4-wave
-//                          long build.
+//                          activations, where it fits in the 4-wave long build (off:
+//                          the second pass's loads already leave right behind the
+//                          first pass's, and it measured no gain).
 //   DL_U_EARLY             load the log values of the next merge chunk before
 //                          contracting the current one.
 #ifndef DL_STAGE_CHUNKS
@@ -209,14 +210,13 @@ __device__ __forceinline__ float dl_exp(float x) { return __expf(x); }
 #ifndef DL_PREFETCH_NEXT_PASS_PER_KEY
 #define DL_PREFETCH_NEXT_PASS_PER_KEY 0
 #endif
-//   DL_PREFETCH_U_LATER    long builds with per-key decay, bf16 activations, an fp32
-//                          state and 8 row groups (128-row heads, whose later values
-//                          start with the second pass; the other builds would spill or
-//                          lose a wave): load
-//                          the first pair of the replay's later log values (entries
-//                          rg + 2 NRG and rg + 3 NRG)
-//                          with the first two, before the first barrier, instead of after
-//                          the coefficient passes.
+//   DL_PREFETCH_U_LATER    load the first pair of the replay's later log values
+//                          (entries rg + 2 NRG and rg + 3 NRG) with the first two, before
+//                          the first barrier, instead of after the coefficient passes.
+//                          Long builds with per-key decay, bf16 activations, an fp32 state
+//                          and 8 row groups only (128-row heads, whose later values start
+//                          with the second pass); the other builds would spill or lose a
+//                          wave.
 #ifndef DL_PREFETCH_U_LATER
 #define DL_PREFETCH_U_LATER 1
 #endif
@@ -1007,10 +1007,10 @@ void deltalog_kernel(KParams p) {
   if constexpr (CF::REPLAYS) {
     constexpr bool kFirstPrefetched = DL_PREFETCH_KEYS && (DL == 1 || kPrefetchPerKey);
     // The next pass is prefetched where the registers allow it at the build's occupancy:
-    // one log-decay per head (a scalar snapshot), small heads, and 128² per-key heads
-    // with bf16 activations (the 4-wave long build; the bonus readout's extra registers
-    // leave room for the keys only).  With fp32 activations or other shapes a 128-row
-    // per-key head would need 12 more registers across the pass (one wave less).
+    // one log-decay per head (a scalar snapshot) or small heads; optionally 128² per-key
+    // heads with bf16 activations (the 4-wave long build; the bonus readout's extra
+    // registers leave room for the keys only).  With fp32 activations or other shapes a
+    // 128-row per-key head would need 12 more registers across the pass (one wave less).
     constexpr int kNextPerKey =
         (sizeof(TIN) == 2 && DK == 128 && DV == 128 && DL_PREFETCH_NEXT_PASS_PER_KEY)
             ? (CF::BONUS ? 2 : DL_PREFETCH_NEXT_PASS) : 0;
