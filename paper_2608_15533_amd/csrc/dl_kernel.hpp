@@ -149,6 +149,13 @@ __device__ __forceinline__ float dl_exp(float x) { return __expf(x); }
 #ifndef DL_NT_STATE
 #define DL_NT_STATE 1
 #endif
+// Cache policy of the state-tile stores alone (the merged base): -1 = as the loads;
+// by default non-temporal with device scope (nt sc1), so that the base is written
+// through the XCD's L2 rather than held there as dirty lines while the other
+// workgroups of the launch stream their tiles in.
+#ifndef DL_STATE_STORE_POLICY
+#define DL_STATE_STORE_POLICY (DL_NT_STATE ? 18 : -1)
+#endif
 // Log keys of the first coefficient pass / the first replay values of each row group
 // are loaded before the first barrier (1) or where they are used (0).
 #ifndef DL_PREFETCH_KEYS
@@ -267,7 +274,9 @@ __device__ __forceinline__ float dl_exp(float x) { return __expf(x); }
 // the row blocks differ by a scalar offset, so no per-row 64-bit addresses occupy
 // vector registers between the load and the store.  The resource covers exactly the
 // head's dk x dv state elements; the hardware drops accesses outside it.
-constexpr int kStateCachePolicy = DL_NT_STATE ? 2 : 0;   // 2 = non-temporal
+constexpr int kStateCachePolicy = DL_NT_STATE ? 2 : 0;   // 2 = non-temporal (nt)
+constexpr int kStateStorePolicy =            // 18 = nt (2) + device scope (sc1, 16)
+    DL_STATE_STORE_POLICY >= 0 ? DL_STATE_STORE_POLICY : kStateCachePolicy;
 constexpr int kRawBufferFlags = 0x00020000;                // 32-bit data format, raw access
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t state_rsrc(void* base, uint32_t bytes) {
@@ -297,7 +306,7 @@ template <> struct StateQuad<float> {
     typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
     const u32x4 x = {__float_as_uint(v.x), __float_as_uint(v.y), __float_as_uint(v.z),
                      __float_as_uint(v.w)};
-    __builtin_amdgcn_raw_buffer_store_b128(x, r, voff, soff, kStateCachePolicy);
+    __builtin_amdgcn_raw_buffer_store_b128(x, r, voff, soff, kStateStorePolicy);
   }
   // The materialised rows at the end of a kernel: the row registers are the store data
   // and nothing writes them afterwards.
@@ -322,7 +331,7 @@ template <> struct StateQuad<uint16_t> {
                                                uint32_t soff, float4 v) {
     typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
     const u32x2 x = {bf16_rne(v.x) | (bf16_rne(v.y) << 16), bf16_rne(v.z) | (bf16_rne(v.w) << 16)};
-    __builtin_amdgcn_raw_buffer_store_b64(x, r, voff, soff, kStateCachePolicy);
+    __builtin_amdgcn_raw_buffer_store_b64(x, r, voff, soff, kStateStorePolicy);
   }
   // The materialised rows at the end of a kernel.
   template <int N>
@@ -659,7 +668,7 @@ struct MfmaMerge<32, RPT> {                       // v_mfma_f32_32x32x2f32
     }
 #pragma unroll
     for (int j = 0; j < 16; ++j)
-      __builtin_amdgcn_raw_buffer_store_b128(x[j], r, voff, j * row_block, kStateCachePolicy);
+      __builtin_amdgcn_raw_buffer_store_b128(x[j], r, voff, j * row_block, kStateStorePolicy);
 #pragma unroll
     for (int j = 0; j < 16; ++j) asm volatile("" ::"v"(x[j]));
   }
@@ -726,7 +735,7 @@ struct MfmaMerge<16, RPT> {                       // v_mfma_f32_16x16x4f32 (64 c
       }
 #pragma unroll
     for (int j = 0; j < RPT; ++j)
-      __builtin_amdgcn_raw_buffer_store_b128(x[j], r, voff, j * row_block, kStateCachePolicy);
+      __builtin_amdgcn_raw_buffer_store_b128(x[j], r, voff, j * row_block, kStateStorePolicy);
 #pragma unroll
     for (int j = 0; j < RPT; ++j) asm volatile("" ::"v"(x[j]));
   }
